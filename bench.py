@@ -1,0 +1,223 @@
+"""Benchmark of one speculative verification step on one MI355X.
+
+A step is the whole hot path over one batch of synthetic inputs resident in HBM:
+  sr_heads_propose (heads + vocabulary projection + draft tree)
+  -> sr_tree_verify_attn (tree-masked attention over the paged prefix, one layer)
+  -> sr_tree_accept (exact acceptance walk).
+Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
+hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
+
+Prints one JSON line. ``--gpus`` above 1 is refused: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "verified tree tokens/s per GPU at 7B shape; tree-attn HBM GB/s % peak"
+HBM_PEAK_GBPS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def dev_tensor(x, device):
+    import numpy as np
+    import torch
+    if x.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+def algorithmic(cfg, ctx_len, kernel):
+    """Algorithmic bytes and flops of one launch of ``kernel`` for this workload."""
+    B, T, Hq, Hkv, D, d, H, V = cfg.B, cfg.T, cfg.Hq, cfg.Hkv, cfg.D, cfg.d, cfg.H, cfg.V
+    e = 2 if cfg.dtype == "bf16" else 4
+    Ls = float(sum(int(x) for x in ctx_len))
+    if kernel == "sr_vocab_gemm":
+        M = B * H
+        return dict(bytes=V * d * e + M * d * e + M * V * 4, flops=2.0 * M * V * d)
+    if kernel == "sr_head_gemm":
+        return dict(bytes=H * d * d * e + H * d * e + B * d * (e + 4) + B * H * d * e, flops=2.0 * B * H * d * d)
+    if kernel == "sr_tree_attn":
+        kv = Ls * 2 * Hkv * D * e
+        return dict(bytes=kv + B * T * (Hq + 2 * Hkv) * D * e + B * T * Hq * (D + 1) * 4,
+                    flops=4.0 * T * Hq * D * Ls)
+    return dict(bytes=float("nan"), flops=float("nan"))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=2, help="trajectories the oracle runs on")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_04962_amd as sr
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cfg = synth.CONFIGS[2]
+    t0 = time.time()
+    hin = synth.heads_inputs(cfg, seed=args.seed)
+    ain = synth.attn_inputs(cfg, seed=args.seed)
+    cin = synth.accept_inputs(cfg, seed=args.seed)
+    log(f"inputs generated in {time.time() - t0:.1f}s")
+
+    H = {k: dev_tensor(hin[k], dev) for k in ("hidden", "corr", "active", "A", "bias", "W", "parents", "root_token",
+                                              "u_tree")}
+    A_ = {k: dev_tensor(ain[k], dev) for k in ("q", "k_cache", "v_cache", "block_table", "ctx_len", "k_tree", "v_tree",
+                                               "parents")}
+    C_ = {k: dev_tensor(cin[k], dev) for k in ("target_logits", "child_logit", "tokens", "parents", "u_acc", "u_fin")}
+    B, T = cfg.B, cfg.T
+    # outputs and workspaces allocated once, outside the timed region
+    tok = torch.empty((B, T), dtype=torch.int32, device=dev)
+    cl = torch.empty((B, T), dtype=torch.float32, device=dev)
+    hws = torch.empty(sr.heads_workspace_bytes(B, cfg.d, cfg.H, cfg.V, T, hin["max_children"]), dtype=torch.uint8,
+                      device=dev)
+    out = torch.empty((B, T, cfg.Hq, cfg.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, T, cfg.Hq), dtype=torch.float32, device=dev)
+    adesc = sr.attn_desc(A_["q"], A_["k_cache"], A_["block_table"])
+    aws_n = sr.attn_workspace_bytes(adesc)
+    aws = torch.empty(max(aws_n, 1), dtype=torch.uint8, device=dev)
+    md = cin["max_depth"]
+    outs = dict(acc_nodes=torch.empty((B, md), dtype=torch.int32, device=dev),
+                out_tokens=torch.empty((B, md + 1), dtype=torch.int32, device=dev),
+                out_len=torch.empty((B,), dtype=torch.int32, device=dev),
+                final_kind=torch.empty((B,), dtype=torch.uint8, device=dev),
+                min_margin=torch.empty((B,), dtype=torch.float32, device=dev))
+
+    def step():
+        sr.heads_propose(H["hidden"], H["corr"], H["active"], H["A"], H["bias"], H["W"], H["parents"],
+                         H["root_token"], H["u_tree"], hin["max_children"], tokens=tok, child_logit=cl,
+                         workspace=hws)
+        sr.tree_verify_attn(A_["q"], A_["k_cache"], A_["v_cache"], A_["block_table"], A_["ctx_len"], A_["k_tree"],
+                            A_["v_tree"], A_["parents"], out=out, lse=lse, workspace=aws)
+        sr.tree_accept(C_["target_logits"], C_["child_logit"], C_["tokens"], C_["parents"], C_["u_acc"],
+                       C_["u_fin"], md, outputs=outs)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # per-kernel durations over the warm-up pattern identify the dominant kernel
+    per_kernel = {}
+    for name in sr.kernel_names():
+        sr.prof_begin(name)
+        step()
+        ms, n = sr.prof_end()
+        if n:
+            per_kernel[name] = ms
+    torch.cuda.synchronize()
+    dominant = max(per_kernel, key=per_kernel.get)
+    log("per-kernel ms (one step): " + ", ".join(f"{k}={v:.4f}" for k, v in per_kernel.items()))
+
+    # timed region: K whole steps; the dominant kernel is bracketed by events on its own stream
+    sr.prof_begin(dominant)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    dom_ms, dom_n = sr.prof_end()
+    ms_per_step = total_ms / args.steps
+    dom_avg_ms = dom_ms / max(dom_n, 1)
+    value = B * T / (ms_per_step / 1e3)
+
+    alg = algorithmic(cfg, ain["ctx_len"], dominant)
+    if dominant in ("sr_vocab_gemm", "sr_head_gemm") and cfg.B * cfg.H >= 312:
+        bound, achieved, peak, unit = "mfma", alg["flops"] / (dom_avg_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", alg["bytes"] / (dom_avg_ms / 1e3) / 1e9, HBM_PEAK_GBPS, "GB/s"
+    attn_alg = algorithmic(cfg, ain["ctx_len"], "sr_tree_attn")
+    attn_ms = per_kernel.get("sr_tree_attn", float("nan")) + per_kernel.get("sr_attn_combine", 0.0)
+    attn_gbps = attn_alg["bytes"] / (attn_ms / 1e3) / 1e9
+
+    # sanity of the step's outputs (not timed)
+    kinds = outs["final_kind"].cpu().numpy()
+    assert (kinds != 255).all(), "invalid trajectories in the benchmark step"
+    assert torch.isfinite(out).all().item()
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "tree tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "7B-shape rollout verification step: B=128 trajectories, 32-node trees (depth 5), "
+                               "Hq=28 Hkv=4 D=128 paged KV (block 16, contexts U[1024,8192]), hidden 3584, "
+                               "4 heads, vocab 151936, one attention layer",
+                   "global_batch": B, "tree_nodes": T, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+                     "traffic": None, "kernel": dominant, "avg_ms": dom_avg_ms, "launches": dom_n},
+        "tree_attn": {"GB/s": attn_gbps, "frac_hbm_peak": attn_gbps / HBM_PEAK_GBPS, "ms": attn_ms},
+        "kernels_ms": per_kernel,
+        "accepted_mean_len": float(outs["out_len"].float().mean().item()),
+    }
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, hin, ain, cin, args.cpu_sample)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(cfg, hin, ain, cin, k):
+    """The float64 oracle on the first k trajectories of the same workload, on the host cores."""
+    import numpy as np
+
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    dt = cfg.dtype
+    rows = np.arange(k)
+    f = lambda x: synth.to_f64(x, dt)
+    A64, b64, W64 = f(hin["A"]), f(hin["bias"]), f(hin["W"])
+    q, kc, vc, kt, vt = (f(ain[n]) for n in ("q", "k_cache", "v_cache", "k_tree", "v_tree"))
+    t0 = time.perf_counter()
+    ho = oracle.heads_forward(f(hin["hidden"])[rows], hin["corr"][rows], hin["active"][rows], A64, b64, W64,
+                              cfg.clip_norm, 1e-5, round_fn=oracle.round_bf16)
+    oracle.tree_build(ho["logits"], hin["parents"][rows], hin["root_token"][rows], hin["u_tree"][rows])
+    t1 = time.perf_counter()
+    oracle.tree_attention(q, kc, vc, ain["block_table"], ain["ctx_len"], kt, vt, ain["parents"], ain["scale"],
+                          nodes=[(int(b), u) for b in rows for u in range(cfg.T)])
+    t2 = time.perf_counter()
+
+    class Rows:
+        def __getitem__(self, b):
+            return f(cin["target_logits"][b])
+    oracle.tree_accept(Rows(), cin["child_logit"], cin["tokens"], cin["parents"], cin["u_acc"], cin["u_fin"], 1.0,
+                       cin["max_depth"], rows=[int(b) for b in rows])
+    t3 = time.perf_counter()
+    secs = t3 - t0
+    return {"value": k * cfg.T / secs, "unit": "tree tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{k} of {cfg.B} trajectories of the same workload (all {cfg.T} nodes each): heads+tree "
+                      f"{t1 - t0:.1f}s, attention {t2 - t1:.1f}s, acceptance {t3 - t2:.1f}s; float64 NumPy",
+            "seconds": secs}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,250 @@
+/*
+ * specroll.h -- C ABI of the MI355X (gfx950) speculative verification step.
+ *
+ * One speculative round for a batch of live trajectories, after SpecRoll
+ * (arXiv 2608.04962):
+ *   1. sr_heads_propose     future-token heads on the last hidden state plus a
+ *                           norm-clipped Reflex correction propose a draft tree
+ *                           (Sec. 3.2 Eq. (heads); App. C "Future-token
+ *                           proposer"; App. B.1 Eq. (slotq), Eq. (childlist)).
+ *      sr_tree_build        the tree-build part of step 1 on given head logits.
+ *   2. sr_tree_verify_attn  target attention of every tree node over its
+ *                           trajectory's paged KV prefix and its own root path
+ *                           (App. B.1 Eq. (nodep)).
+ *   3. sr_tree_accept       exact node-wise speculative acceptance walk
+ *                           (App. B.2 Eq. (nodeaccept), Eq. (noderesidual),
+ *                           Alg. "Exact node-wise tree verification").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers named in an argument list are DEVICE pointers unless stated
+ *   otherwise; descriptors are HOST pointers. All arrays are dense, row-major,
+ *   in the layout given. The caller owns every buffer; the library allocates no
+ *   device memory and keeps no per-call state.
+ * - `stream` is a hipStream_t (NULL = the null stream). Work is enqueued and the
+ *   call returns without synchronising; faults inside kernels surface at the
+ *   caller's next synchronisation.
+ * - `workspace` is device scratch of at least the size the matching
+ *   *_workspace query returns (which may be 0, and then `workspace` may be NULL).
+ * - Arguments are checked on the host before anything is enqueued. A failed
+ *   check returns a non-zero sr_status, leaves every output untouched and sets a
+ *   thread-local message readable through sr_last_error().
+ * - Values that live on the device (parents, ctx_len, block ids, tokens) are
+ *   checked by the kernels themselves; a trajectory whose device-side inputs are
+ *   malformed gets the "invalid" outputs each call documents, never an
+ *   out-of-bounds access.
+ * - Tree topology: parents[b][0] == -1 and 0 <= parents[b][c] < c for c >= 1.
+ *   The children of a node, in increasing node index, are its slots 1..m.
+ *   T <= SR_MAX_TREE.
+ * - Element types: SR_F32 or SR_BF16 (bfloat16 stored as 16-bit patterns).
+ *   Matrix products take bf16 operands with fp32 accumulation, or fp32
+ *   operands with fp32 accumulation.
+ */
+#ifndef SPECROLL_H
+#define SPECROLL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SR_MAX_TREE 128
+
+typedef enum {
+  SR_OK = 0,
+  SR_ERR_INVALID = 1,      /* bad descriptor, null pointer or shape          */
+  SR_ERR_UNSUPPORTED = 2,  /* valid request outside the built kernel set     */
+  SR_ERR_WORKSPACE = 3,    /* workspace missing or smaller than required     */
+  SR_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed     */
+} sr_status;
+
+typedef enum { SR_F32 = 0, SR_BF16 = 1 } sr_dtype;
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* sr_last_error(void);
+/* Library version string. */
+const char* sr_version(void);
+
+/* ========================================================================== *
+ * 1. Proposal: heads + tree build
+ * ========================================================================== *
+ * For every trajectory b (Sec. 3.2 Eq. (heads); App. C):
+ *   D'_b  = active_b ? corr_b * min(1, clip_norm / ||corr_b||_2) : 0
+ *           (a zero correction stays zero)
+ *   x_b   = hidden_b + D'_b                                       (fp32)
+ *   n_b   = LayerNorm(x_b), biased variance, eps = ln_eps, no affine;
+ *           rounded to `dtype`
+ *   z_b,h = x_b + SiLU(A_h n_b + bias_h),  h = 1..H;  rounded to `dtype`
+ *   logits_b,h = W z_b,h                                           (fp32)
+ * then the draft tree (App. B.1): node u at depth d is proposed from by head
+ * k = min(d + 1, H). With m_u children, C_u = the m_u largest entries of
+ * logits_b,k ordered by (logit descending, token id ascending). The children
+ * of u fill slots 1..m_u in index order; slot j draws without replacement from
+ * the not-yet-drawn part R of C_u with weights exp(l_v - max_R l), by inverse
+ * CDF over R in C_u's order: the first v with U * S < cumulative weight
+ * through v, S the total, U = u_tree[b][child]. Weights and sums are float64.
+ */
+typedef struct {
+  int32_t B;             /* trajectories, >= 1                                */
+  int32_t d;             /* hidden size, multiple of 64                       */
+  int32_t H;             /* future-token heads, >= 1                          */
+  int32_t V;             /* vocabulary, >= max_children                       */
+  int32_t T;             /* tree nodes incl. the root, 1..SR_MAX_TREE         */
+  int32_t max_children;  /* upper bound on any node's child count, 0..T-1     */
+  sr_dtype dtype;        /* element type of hidden, A, bias, W and z          */
+  float clip_norm;       /* L2 bound c of the Reflex correction, > 0          */
+  float ln_eps;          /* LayerNorm epsilon, >= 0                           */
+} sr_heads_desc;
+
+size_t sr_heads_propose_workspace(const sr_heads_desc* desc);
+
+/*
+ * hidden      [B,d]    dtype   last hidden state h_t of each trajectory
+ * corr        [B,d]    fp32    Reflex correction vector (NULL = none)
+ * corr_active [B]      uint8   nonzero = apply corr (NULL = all active)
+ * A           [H,d,d]  dtype   head matrices, A[h][out][in]
+ * bias        [H,d]    dtype
+ * W           [V,d]    dtype   shared vocabulary projection (row = token)
+ * parents     [B,T]    int32   tree topology (see conventions)
+ * root_token  [B]      int32   the anchor token, already sampled
+ * u_tree      [B,T]    fp32    uniforms in (0,1); entry c orders the slot node c fills
+ * logits      [B,H,V]  fp32    OUT (optional, NULL = keep in workspace)
+ * z           [B,H,d]  dtype   OUT (optional, NULL = keep in workspace)
+ * tokens      [B,T]    int32   OUT; tokens[b][0] = root_token[b]
+ * child_logit [B,T]    fp32    OUT; head logit of tokens[b][c] under the proposing
+ *                              head; 0 at the root
+ * Invalid trajectory (bad topology, more than max_children children at a node):
+ * its tokens are -1 and child_logit NaN for every non-root node.
+ */
+sr_status sr_heads_propose(const sr_heads_desc* desc,
+                           const void* hidden, const float* corr, const uint8_t* corr_active,
+                           const void* A, const void* bias, const void* W,
+                           const int32_t* parents, const int32_t* root_token, const float* u_tree,
+                           float* logits, void* z, int32_t* tokens, float* child_logit,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Tree build alone (the second half of sr_heads_propose) on caller-supplied fp32
+ * head logits [B,H,V]; desc->d, dtype, clip_norm and ln_eps are ignored. */
+size_t sr_tree_build_workspace(const sr_heads_desc* desc);
+sr_status sr_tree_build(const sr_heads_desc* desc, const float* logits,
+                        const int32_t* parents, const int32_t* root_token, const float* u_tree,
+                        int32_t* tokens, float* child_logit,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ========================================================================== *
+ * 2. Tree-verify attention (App. B.1 Eq. (nodep))
+ * ========================================================================== *
+ * For trajectory b, node u and query head h (KV head g = h / (Hq/Hkv)):
+ *   keys   = prefix tokens 0..ctx_len[b]-1 from the paged cache, then the tree
+ *            tokens on u's root path (ancestors and u itself)
+ *   out[b][u][h] = softmax(scale * q . K^T) V,   lse[b][u][h] = logsumexp(scale * q . K^T)
+ * which equals ordinary causal attention at u's position of the sequence
+ * prefix ++ path(u). Scores and softmax are fp32. For bf16 inputs the
+ * probability-weighted sum over V runs on fp16 matrix cores: V entries are
+ * converted bf16 -> fp16 (exact for |v| in [2^-14, 65504]; smaller magnitudes
+ * lose relative precision, larger ones overflow to inf).
+ */
+typedef struct {
+  int32_t B, T;          /* trajectories; tree nodes (1..SR_MAX_TREE)           */
+  int32_t Hq, Hkv;       /* query / KV heads; Hq % Hkv == 0                     */
+  int32_t D;             /* head dim: 64 or 128                                 */
+  int32_t block_size;    /* tokens per KV page: 16                              */
+  int32_t max_blocks;    /* columns of block_table                              */
+  int32_t num_blocks;    /* pages in k_cache / v_cache                          */
+  sr_dtype dtype;        /* element type of q, caches and tree K/V              */
+  float scale;           /* score scale, usually 1/sqrt(D)                      */
+} sr_attn_desc;
+
+size_t sr_tree_verify_attn_workspace(const sr_attn_desc* desc);
+
+/*
+ * q           [B,T,Hq,D]                         dtype  queries of the tree nodes (positions applied)
+ * k_cache     [num_blocks,Hkv,block_size,D]      dtype  paged prefix keys
+ * v_cache     [num_blocks,Hkv,block_size,D]      dtype  paged prefix values
+ * block_table [B,max_blocks]                     int32  physical page of logical page i
+ * ctx_len     [B]                                int32  prefix tokens in the cache, 0..max_blocks*block_size
+ * k_tree      [B,T,Hkv,D]                        dtype  keys of the tree tokens (node order)
+ * v_tree      [B,T,Hkv,D]                        dtype  values of the tree tokens
+ * parents     [B,T]                              int32  tree topology
+ * out         [B,T,Hq,D]                         fp32   OUT
+ * lse         [B,T,Hq]                           fp32   OUT (optional, NULL = not written)
+ * Cache slots past ctx_len in a trajectory's last page are never read, nor are
+ * block_table entries past its last page. Invalid trajectory (ctx_len out of
+ * range, a page id outside [0,num_blocks), bad topology): out and lse are NaN.
+ */
+sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
+                              const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* block_table, const int32_t* ctx_len,
+                              const void* k_tree, const void* v_tree, const int32_t* parents,
+                              float* out, float* lse,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* ========================================================================== *
+ * 3. Exact acceptance walk (App. B.2)
+ * ========================================================================== *
+ * Per trajectory, starting at the root u: p_u = softmax(target_logits[b][u] /
+ * temperature), r = p_u. For the children c of u in slot order: y = tokens[c],
+ * q = softmax of child_logit over the children not yet tried, accept iff
+ * u_acc[b][c] <= min(1, r(y)/q(y)); on rejection r <- [r - q]_+ / Z over the
+ * whole vocabulary. An accepted child with children is visited next; an
+ * accepted leaf adds a bonus token drawn from its own p; if every child of a
+ * node is rejected, a fallback token is drawn from the final residual. Draws use
+ * the inverse CDF in token-id order with U = u_fin[b]: the first v with
+ * U * S < sum_{w<=v} r(w). Walk scalars are float64; exponentials are fp32 of
+ * (logit - running max) * (1/temperature), summed in float64.
+ * The children of one node must carry distinct tokens.
+ */
+typedef struct {
+  int32_t B, T, V;       /* trajectories; tree nodes (1..SR_MAX_TREE); vocabulary */
+  int32_t max_depth;     /* columns of acc_nodes, >= the deepest node's depth    */
+  sr_dtype logit_dtype;  /* element type of target_logits                        */
+  float temperature;     /* > 0                                                  */
+} sr_accept_desc;
+
+size_t sr_tree_accept_workspace(const sr_accept_desc* desc);
+
+/*
+ * target_logits [B,T,V]           dtype  row u = target logits after prefix ++ path(u)
+ * child_logit   [B,T]             fp32   draft logit of each node's token (entry 0 unused)
+ * tokens        [B,T]             int32  token of each node (entry 0 = the anchor, unused)
+ * parents       [B,T]             int32  tree topology
+ * u_acc         [B,T]             fp32   uniform of the slot test of node c (entry 0 unused)
+ * u_fin         [B]               fp32   uniform of the terminal draw
+ * acc_nodes     [B,max_depth]     int32  OUT accepted node ids in walk order, -1 padded
+ * out_tokens    [B,max_depth+1]   int32  OUT accepted tokens then the terminal token, -1 padded
+ * out_len       [B]               int32  OUT accepted count + 1
+ * final_kind    [B]               uint8  OUT 0 = fallback, 1 = bonus, 255 = invalid input
+ * min_margin    [B]               fp32   OUT (optional) smallest decision margin of the walk:
+ *                                        |min(1,r/q) - U| for slot tests, distance of U*S to the
+ *                                        drawn token's cumulative boundaries / S for draws
+ * Invalid trajectory (bad topology, a token outside [0,V), duplicate sibling
+ * tokens, depth > max_depth): acc_nodes/out_tokens -1, out_len 0, final_kind 255.
+ */
+sr_status sr_tree_accept(const sr_accept_desc* desc,
+                         const void* target_logits, const float* child_logit,
+                         const int32_t* tokens, const int32_t* parents,
+                         const float* u_acc, const float* u_fin,
+                         int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len,
+                         uint8_t* final_kind, float* min_margin,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ========================================================================== *
+ * Kernel timing hook
+ * ========================================================================== *
+ * Between sr_prof_begin and sr_prof_end, every launch of the kernel whose name
+ * contains `kernel_substr` is bracketed by a pair of HIP events on its own
+ * stream (at most 4096 launches). sr_prof_end synchronises those events and
+ * returns the summed duration in milliseconds and the launch count. Kernel names
+ * are listed by sr_kernel_names (a ';'-separated host string). Not thread-safe.
+ */
+sr_status sr_prof_begin(const char* kernel_substr);
+sr_status sr_prof_end(double* total_ms, int32_t* launches);
+const char* sr_kernel_names(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECROLL_H */

@@ -56,7 +56,8 @@ def heads_forward(hidden: np.ndarray, corr: Optional[np.ndarray], active: Option
 
     hidden [B,d], corr [B,d] (None = no correction), active [B] (None = all active),
     A [H,d,d] with A[h][out][in], bias [H,d], W [V,d] (row = token).
-    Returns x [B,d], n [B,d], z [B,H,d] and logits [B,H,V] (float64).
+    Returns x [B,d], n [B,d], z [B,H,d] and logits [B,H,V] (float64); ``z_exact`` is z before its
+    rounding point (equal to z when ``round_fn`` is None).
     """
     hidden = np.asarray(hidden, dtype=np.float64)
     B, d = hidden.shape
@@ -70,11 +71,13 @@ def heads_forward(hidden: np.ndarray, corr: Optional[np.ndarray], active: Option
     if round_fn is not None:
         n = round_fn(n)
     z = np.empty((B, H, d), dtype=np.float64)
+    z_exact = np.empty((B, H, d), dtype=np.float64)
     for h in range(H):
         a = n @ np.asarray(A[h], dtype=np.float64).T + np.asarray(bias[h], dtype=np.float64)
         zh = x + silu(a)
+        z_exact[:, h, :] = zh
         z[:, h, :] = round_fn(zh) if round_fn is not None else zh
-    out = dict(x=x, n=n, z=z)
+    out = dict(x=x, n=n, z=z, z_exact=z_exact)
     if with_logits:
         W64 = np.asarray(W, dtype=np.float64)
         out["logits"] = np.einsum("bhd,vd->bhv", z, W64, optimize=True)

@@ -1,0 +1,230 @@
+"""MI355X (gfx950) speculative verification step after SpecRoll (arXiv 2608.04962).
+
+Thin torch-tensor binding over the C ABI of ``libspecroll.so`` (include/specroll.h):
+argument marshalling only; every step runs in the HIP kernels. PyTorch supplies device
+memory and the current stream.
+
+    heads_propose     future-token heads + draft tree      (Sec. 3.2 Eq. (heads); App. B.1)
+    tree_build        the tree-build half on given head logits
+    tree_verify_attn  tree-masked attention over the paged prefix (App. B.1 Eq. (nodep))
+    tree_accept       exact node-wise acceptance walk      (App. B.2)
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+from typing import Optional
+
+import torch
+
+from . import _lib
+from ._lib import AcceptDesc, AttnDesc, HeadsDesc, SpecRollError, check, lib  # noqa: F401
+
+__all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "prof_begin", "prof_end",
+           "kernel_names", "version", "SpecRollError", "library_path"]
+
+_DT = {torch.float32: _lib.SR_F32, torch.bfloat16: _lib.SR_BF16}
+
+
+def library_path() -> str:
+    return _lib.LIB_PATH
+
+
+def version() -> str:
+    return lib().sr_version().decode()
+
+
+def kernel_names():
+    return lib().sr_kernel_names().decode().split(";")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t, name, dtype, shape, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    if nbytes == 0:
+        return None, 0
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError(f"workspace holds {workspace.numel() * workspace.element_size()} bytes, {nbytes} needed")
+        return workspace, workspace.numel() * workspace.element_size()
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return ws, nbytes
+
+
+def heads_workspace_bytes(B, d, H, V, T, max_children, dtype=torch.bfloat16) -> int:
+    desc = HeadsDesc(B, d, H, V, T, max_children, _DT[dtype], 1.0, 1e-5)
+    return int(lib().sr_heads_propose_workspace(C.byref(desc)))
+
+
+def heads_propose(hidden, corr, corr_active, A, bias, W, parents, root_token, u_tree, max_children: int,
+                  clip_norm: float = 1.0, ln_eps: float = 1e-5, logits: Optional[torch.Tensor] = None,
+                  z: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
+                  child_logit: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """Heads on the corrected hidden state, shared-vocabulary logits and the draft tree.
+
+    hidden [B,d] bf16|f32, corr [B,d] f32 or None, corr_active [B] uint8 or None, A [H,d,d],
+    bias [H,d], W [V,d] (same dtype as hidden), parents [B,T] int32, root_token [B] int32,
+    u_tree [B,T] f32. ``logits`` [B,H,V] f32 and ``z`` [B,H,d] are optional outputs.
+    Returns (tokens [B,T] int32, child_logit [B,T] f32).
+    """
+    dev = hidden.device
+    B, d = hidden.shape
+    H = A.shape[0]
+    V = W.shape[0]
+    T = parents.shape[1]
+    dt = hidden.dtype
+    _need(hidden, "hidden", None, (B, d), dev)
+    if dt not in _DT:
+        raise TypeError("hidden must be float32 or bfloat16")
+    if corr is not None:
+        _need(corr, "corr", torch.float32, (B, d), dev)
+    if corr_active is not None:
+        _need(corr_active, "corr_active", torch.uint8, (B,), dev)
+    _need(A, "A", dt, (H, d, d), dev)
+    _need(bias, "bias", dt, (H, d), dev)
+    _need(W, "W", dt, (V, d), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    _need(root_token, "root_token", torch.int32, (B,), dev)
+    _need(u_tree, "u_tree", torch.float32, (B, T), dev)
+    if logits is not None:
+        _need(logits, "logits", torch.float32, (B, H, V), dev)
+    if z is not None:
+        _need(z, "z", dt, (B, H, d), dev)
+    tokens = torch.empty((B, T), dtype=torch.int32, device=dev) if tokens is None else tokens
+    child_logit = torch.empty((B, T), dtype=torch.float32, device=dev) if child_logit is None else child_logit
+    _need(tokens, "tokens", torch.int32, (B, T), dev)
+    _need(child_logit, "child_logit", torch.float32, (B, T), dev)
+    desc = HeadsDesc(B, d, H, V, T, int(max_children), _DT[dt], float(clip_norm), float(ln_eps))
+    ws, wsb = _workspace(int(lib().sr_heads_propose_workspace(C.byref(desc))), dev, workspace)
+    st = lib().sr_heads_propose(C.byref(desc), _ptr(hidden), _ptr(corr), _ptr(corr_active), _ptr(A), _ptr(bias),
+                                _ptr(W), _ptr(parents), _ptr(root_token), _ptr(u_tree), _ptr(logits), _ptr(z),
+                                _ptr(tokens), _ptr(child_logit), _ptr(ws), wsb, _stream(dev))
+    check(st, "sr_heads_propose")
+    return tokens, child_logit
+
+
+def tree_build(logits, parents, root_token, u_tree, max_children: int, tokens=None, child_logit=None,
+               workspace=None):
+    """Draft tree from fp32 head logits [B,H,V]. Returns (tokens, child_logit)."""
+    dev = logits.device
+    B, H, V = logits.shape
+    T = parents.shape[1]
+    _need(logits, "logits", torch.float32, (B, H, V), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    _need(root_token, "root_token", torch.int32, (B,), dev)
+    _need(u_tree, "u_tree", torch.float32, (B, T), dev)
+    tokens = torch.empty((B, T), dtype=torch.int32, device=dev) if tokens is None else tokens
+    child_logit = torch.empty((B, T), dtype=torch.float32, device=dev) if child_logit is None else child_logit
+    desc = HeadsDesc(B, 0, H, V, T, int(max_children), _lib.SR_F32, 1.0, 0.0)
+    ws, wsb = _workspace(int(lib().sr_tree_build_workspace(C.byref(desc))), dev, workspace)
+    st = lib().sr_tree_build(C.byref(desc), _ptr(logits), _ptr(parents), _ptr(root_token), _ptr(u_tree),
+                             _ptr(tokens), _ptr(child_logit), _ptr(ws), wsb, _stream(dev))
+    check(st, "sr_tree_build")
+    return tokens, child_logit
+
+
+def attn_desc(q, k_cache, block_table, scale=None) -> AttnDesc:
+    B, T, Hq, D = q.shape
+    NB, Hkv, bs, D2 = k_cache.shape
+    return AttnDesc(B, T, Hq, Hkv, D, bs, block_table.shape[1], NB, _DT[q.dtype],
+                    float(1.0 / math.sqrt(D) if scale is None else scale))
+
+
+def attn_workspace_bytes(desc: AttnDesc) -> int:
+    return int(lib().sr_tree_verify_attn_workspace(C.byref(desc)))
+
+
+def tree_verify_attn(q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, scale=None,
+                     out=None, lse=None, want_lse: bool = True, workspace=None):
+    """Tree-masked attention. q [B,T,Hq,D], caches [NB,Hkv,16,D], block_table [B,max_blocks] int32,
+    ctx_len [B] int32, k_tree/v_tree [B,T,Hkv,D], parents [B,T] int32. Returns (out fp32, lse fp32 or None)."""
+    dev = q.device
+    B, T, Hq, D = q.shape
+    NB, Hkv, bs, _ = k_cache.shape
+    dt = q.dtype
+    _need(q, "q", None, (B, T, Hq, D), dev)
+    if dt not in _DT:
+        raise TypeError("q must be float32 or bfloat16")
+    _need(k_cache, "k_cache", dt, (NB, Hkv, bs, D), dev)
+    _need(v_cache, "v_cache", dt, (NB, Hkv, bs, D), dev)
+    _need(block_table, "block_table", torch.int32, (B, block_table.shape[1]), dev)
+    _need(ctx_len, "ctx_len", torch.int32, (B,), dev)
+    _need(k_tree, "k_tree", dt, (B, T, Hkv, D), dev)
+    _need(v_tree, "v_tree", dt, (B, T, Hkv, D), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    out = torch.empty((B, T, Hq, D), dtype=torch.float32, device=dev) if out is None else out
+    _need(out, "out", torch.float32, (B, T, Hq, D), dev)
+    if want_lse and lse is None:
+        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=dev)
+    desc = attn_desc(q, k_cache, block_table, scale)
+    ws, wsb = _workspace(attn_workspace_bytes(desc), dev, workspace)
+    st = lib().sr_tree_verify_attn(C.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                   _ptr(ctx_len), _ptr(k_tree), _ptr(v_tree), _ptr(parents), _ptr(out),
+                                   _ptr(lse), _ptr(ws), wsb, _stream(dev))
+    check(st, "sr_tree_verify_attn")
+    return out, lse
+
+
+def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, max_depth: int,
+                temperature: float = 1.0, outputs: Optional[dict] = None, want_margin: bool = True):
+    """Exact acceptance walk. target_logits [B,T,V] bf16|f32; child_logit [B,T] f32; tokens, parents [B,T]
+    int32; u_acc [B,T] f32; u_fin [B] f32. Returns dict(acc_nodes, out_tokens, out_len, final_kind, min_margin)."""
+    dev = target_logits.device
+    B, T, V = target_logits.shape
+    dt = target_logits.dtype
+    if dt not in _DT:
+        raise TypeError("target_logits must be float32 or bfloat16")
+    _need(target_logits, "target_logits", dt, (B, T, V), dev)
+    _need(child_logit, "child_logit", torch.float32, (B, T), dev)
+    _need(tokens, "tokens", torch.int32, (B, T), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    _need(u_acc, "u_acc", torch.float32, (B, T), dev)
+    _need(u_fin, "u_fin", torch.float32, (B,), dev)
+    if outputs is None:
+        outputs = dict(
+            acc_nodes=torch.empty((B, max(max_depth, 1)), dtype=torch.int32, device=dev),
+            out_tokens=torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev),
+            out_len=torch.empty((B,), dtype=torch.int32, device=dev),
+            final_kind=torch.empty((B,), dtype=torch.uint8, device=dev),
+            min_margin=torch.empty((B,), dtype=torch.float32, device=dev) if want_margin else None,
+        )
+    desc = AcceptDesc(B, T, V, int(max_depth), _DT[dt], float(temperature))
+    st = lib().sr_tree_accept(C.byref(desc), _ptr(target_logits), _ptr(child_logit), _ptr(tokens), _ptr(parents),
+                              _ptr(u_acc), _ptr(u_fin), _ptr(outputs["acc_nodes"]), _ptr(outputs["out_tokens"]),
+                              _ptr(outputs["out_len"]), _ptr(outputs["final_kind"]), _ptr(outputs["min_margin"]),
+                              None, 0, _stream(dev))
+    check(st, "sr_tree_accept")
+    if max_depth == 0:
+        outputs["acc_nodes"] = outputs["acc_nodes"][:, :0]
+    return outputs
+
+
+def prof_begin(kernel_substr: str) -> None:
+    check(lib().sr_prof_begin(kernel_substr.encode()), "sr_prof_begin")
+
+
+def prof_end():
+    """Returns (total_ms, launches) of the kernel selected by prof_begin."""
+    ms = C.c_double()
+    n = C.c_int32()
+    check(lib().sr_prof_end(C.byref(ms), C.byref(n)), "sr_prof_end")
+    return ms.value, n.value

@@ -1,0 +1,303 @@
+// C ABI of the speculative verification step: argument checks, workspace layout,
+// error reporting and the kernel timing hook. Compute lives in k_*.hip.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <cmath>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace sr {
+
+static thread_local std::string g_err;
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+}
+
+sr_status hip_fail(hipError_t e, const char* what) {
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return SR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------- timing hook
+struct Prof {
+  bool on = false;
+  std::string pat;
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+  static constexpr int kMax = 4096;
+};
+static Prof g_prof;
+
+LaunchGuard::LaunchGuard(const char* n, hipStream_t s) : name(n), stream(s), slot(-1) {
+  if (g_prof.on && strstr(n, g_prof.pat.c_str()) != nullptr && g_prof.used < Prof::kMax) {
+    if ((int)g_prof.start.size() <= g_prof.used) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+      g_prof.start.push_back(a);
+      g_prof.stop.push_back(b);
+    }
+    slot = g_prof.used;
+    (void)hipEventRecord(g_prof.start[slot], s);
+  }
+}
+
+sr_status LaunchGuard::done() {
+  hipError_t e = hipGetLastError();
+  if (slot >= 0) {
+    (void)hipEventRecord(g_prof.stop[slot], stream);
+    ++g_prof.used;
+  }
+  if (e != hipSuccess) {
+    set_error("launch of %s failed: %s", name, hipGetErrorString(e));
+    return SR_ERR_HIP;
+  }
+  return SR_OK;
+}
+
+// ---------------------------------------------------------------- helpers
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+static size_t esize(sr_dtype t) { return t == SR_BF16 ? 2 : 4; }
+static bool dtype_ok(sr_dtype t) { return t == SR_F32 || t == SR_BF16; }
+
+#define SR_CHECK(cond, ...)        \
+  do {                             \
+    if (!(cond)) {                 \
+      ::sr::set_error(__VA_ARGS__); \
+      return SR_ERR_INVALID;       \
+    }                              \
+  } while (0)
+
+struct HeadsLayout {
+  size_t x, n, z, logits, top_id, top_val, total;
+};
+static HeadsLayout heads_layout(const sr_heads_desc& d, bool need_z, bool need_logits) {
+  HeadsLayout L;
+  size_t off = 0;
+  const size_t B = d.B, H = d.H, dd = d.d, V = d.V, M = d.max_children;
+  L.x = off; off = align_up(off + B * dd * 4);
+  L.n = off; off = align_up(off + B * dd * esize(d.dtype));
+  L.z = off; if (need_z) off = align_up(off + B * H * dd * esize(d.dtype));
+  L.logits = off; if (need_logits) off = align_up(off + B * H * V * 4);
+  L.top_id = off; off = align_up(off + B * H * M * 4);
+  L.top_val = off; off = align_up(off + B * H * M * 4);
+  L.total = off;
+  return L;
+}
+
+static sr_status check_heads_desc(const sr_heads_desc* d, bool tree_only) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(d->B >= 1, "B must be >= 1 (got %d)", d->B);
+  SR_CHECK(d->H >= 1, "H must be >= 1 (got %d)", d->H);
+  SR_CHECK(d->V >= 1, "V must be >= 1 (got %d)", d->V);
+  SR_CHECK(d->T >= 1 && d->T <= SR_MAX_TREE, "T must be in [1, %d] (got %d)", SR_MAX_TREE, d->T);
+  SR_CHECK(d->max_children >= 0 && d->max_children <= d->T - 1, "max_children must be in [0, T-1] (got %d)",
+           d->max_children);
+  SR_CHECK(d->T == 1 || d->max_children >= 1, "a tree with T > 1 needs max_children >= 1");
+  SR_CHECK(d->max_children <= d->V, "max_children (%d) exceeds V (%d)", d->max_children, d->V);
+  if (!tree_only) {
+    SR_CHECK(d->d >= 64 && d->d % 64 == 0, "d must be a positive multiple of 64 (got %d)", d->d);
+    SR_CHECK(dtype_ok(d->dtype), "unknown dtype %d", (int)d->dtype);
+    SR_CHECK(std::isfinite(d->clip_norm) && d->clip_norm > 0.f, "clip_norm must be finite and > 0");
+    SR_CHECK(std::isfinite(d->ln_eps) && d->ln_eps >= 0.f, "ln_eps must be finite and >= 0");
+    SR_CHECK((size_t)d->H * d->d <= (size_t)INT32_MAX, "H*d too large");
+  }
+  SR_CHECK((size_t)d->B * d->H <= (size_t)INT32_MAX, "B*H too large");
+  return SR_OK;
+}
+
+static sr_status check_ws(const void* ws, size_t have, size_t need) {
+  if (need == 0) return SR_OK;
+  if (ws == nullptr || have < need) {
+    set_error("workspace of %zu bytes required, %zu given%s", need, have, ws ? "" : " (null)");
+    return SR_ERR_WORKSPACE;
+  }
+  if (((uintptr_t)ws & 255u) != 0) {
+    set_error("workspace must be 256-byte aligned");
+    return SR_ERR_INVALID;
+  }
+  return SR_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace sr
+
+using namespace sr;
+
+extern "C" {
+
+const char* sr_last_error(void) { return g_err.c_str(); }
+
+const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
+
+const char* sr_kernel_names(void) {
+  return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_topm;sr_tree_build;sr_tree_attn;sr_attn_combine;sr_tree_accept";
+}
+
+// ------------------------------------------------------------------ proposal
+size_t sr_heads_propose_workspace(const sr_heads_desc* d) {
+  if (check_heads_desc(d, false) != SR_OK) return 0;
+  return heads_layout(*d, true, true).total;
+}
+
+sr_status sr_heads_propose(const sr_heads_desc* d, const void* hidden, const float* corr, const uint8_t* corr_active,
+                           const void* A, const void* bias, const void* W, const int32_t* parents,
+                           const int32_t* root_token, const float* u_tree, float* logits, void* z, int32_t* tokens,
+                           float* child_logit, void* workspace, size_t workspace_bytes, void* stream) {
+  sr_status st = check_heads_desc(d, false);
+  if (st != SR_OK) return st;
+  SR_CHECK(hidden && A && bias && W && parents && root_token && u_tree && tokens && child_logit,
+           "a required pointer is null");
+  SR_CHECK(aligned16(hidden) && aligned16(A) && aligned16(W) && aligned16(bias), "hidden/A/bias/W must be 16-byte aligned");
+  SR_CHECK(z == nullptr || aligned16(z), "z must be 16-byte aligned");
+  const HeadsLayout L = heads_layout(*d, z == nullptr, logits == nullptr);
+  st = check_ws(workspace, workspace_bytes, L.total);
+  if (st != SR_OK) return st;
+  char* ws = (char*)workspace;
+  float* x = (float*)(ws + L.x);
+  void* n = ws + L.n;
+  void* zz = z ? z : (void*)(ws + L.z);
+  float* lg = logits ? logits : (float*)(ws + L.logits);
+  hipStream_t s = (hipStream_t)stream;
+  st = launch_heads(*d, hidden, corr, corr_active, A, bias, W, x, n, zz, lg, s);
+  if (st != SR_OK) return st;
+  return launch_tree_build(*d, lg, parents, root_token, u_tree, tokens, child_logit, (int32_t*)(ws + L.top_id),
+                           (float*)(ws + L.top_val), s);
+}
+
+size_t sr_tree_build_workspace(const sr_heads_desc* d) {
+  if (check_heads_desc(d, true) != SR_OK) return 0;
+  const size_t n = (size_t)d->B * d->H * d->max_children * 4;
+  return 2 * align_up(n);
+}
+
+sr_status sr_tree_build(const sr_heads_desc* d, const float* logits, const int32_t* parents,
+                        const int32_t* root_token, const float* u_tree, int32_t* tokens, float* child_logit,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  sr_status st = check_heads_desc(d, true);
+  if (st != SR_OK) return st;
+  SR_CHECK(logits && parents && root_token && u_tree && tokens && child_logit, "a required pointer is null");
+  const size_t n = align_up((size_t)d->B * d->H * d->max_children * 4);
+  st = check_ws(workspace, workspace_bytes, 2 * n);
+  if (st != SR_OK) return st;
+  char* ws = (char*)workspace;
+  return launch_tree_build(*d, logits, parents, root_token, u_tree, tokens, child_logit, (int32_t*)ws,
+                           (float*)(ws + n), (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ attention
+static sr_status check_attn_desc(const sr_attn_desc* d) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(d->B >= 1 && d->B <= 65535, "B must be in [1, 65535] (got %d)", d->B);
+  SR_CHECK(d->T >= 1 && d->T <= SR_MAX_TREE, "T must be in [1, %d] (got %d)", SR_MAX_TREE, d->T);
+  SR_CHECK(d->Hkv <= 65535, "Hkv too large");
+  SR_CHECK(d->Hq >= 1 && d->Hkv >= 1 && d->Hq % d->Hkv == 0, "need Hq >= 1, Hkv >= 1 and Hq %% Hkv == 0");
+  SR_CHECK(d->D == 64 || d->D == 128, "D must be 64 or 128 (got %d)", d->D);
+  SR_CHECK(d->block_size == 16, "block_size must be 16 (got %d)", d->block_size);
+  SR_CHECK(d->max_blocks >= 1 && d->num_blocks >= 1, "max_blocks and num_blocks must be >= 1");
+  SR_CHECK((size_t)d->max_blocks * 16 <= (size_t)INT32_MAX / 2, "max_blocks too large");
+  SR_CHECK(dtype_ok(d->dtype), "unknown dtype %d", (int)d->dtype);
+  SR_CHECK(std::isfinite(d->scale), "scale must be finite");
+  return SR_OK;
+}
+
+size_t sr_tree_verify_attn_workspace(const sr_attn_desc* d) {
+  if (check_attn_desc(d) != SR_OK) return 0;
+  const AttnPlan p = attn_plan(*d);
+  return align_up(p.part_o_bytes) + align_up(p.part_ml_bytes);
+}
+
+sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
+                              const void* v_tree, const int32_t* parents, float* out, float* lse, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  sr_status st = check_attn_desc(d);
+  if (st != SR_OK) return st;
+  SR_CHECK(q && k_cache && v_cache && block_table && ctx_len && k_tree && v_tree && parents && out,
+           "a required pointer is null");
+  SR_CHECK(aligned16(q) && aligned16(k_cache) && aligned16(v_cache) && aligned16(k_tree) && aligned16(v_tree) &&
+               aligned16(out),
+           "q, caches, tree K/V and out must be 16-byte aligned");
+  const AttnPlan p = attn_plan(*d);
+  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes);
+  st = check_ws(workspace, workspace_bytes, need);
+  if (st != SR_OK) return st;
+  char* ws = (char*)workspace;
+  float* po = need ? (float*)ws : nullptr;
+  float* pml = need ? (float*)(ws + align_up(p.part_o_bytes)) : nullptr;
+  return launch_tree_attn(*d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse, po,
+                          pml, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ acceptance
+static sr_status check_accept_desc(const sr_accept_desc* d) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(d->B >= 1, "B must be >= 1 (got %d)", d->B);
+  SR_CHECK(d->T >= 1 && d->T <= SR_MAX_TREE, "T must be in [1, %d] (got %d)", SR_MAX_TREE, d->T);
+  SR_CHECK(d->V >= 8 && d->V <= 262144 && d->V % 8 == 0, "V must be a multiple of 8 in [8, 262144] (got %d)", d->V);
+  SR_CHECK(d->max_depth >= 0 && d->max_depth <= SR_MAX_TREE, "max_depth must be in [0, %d]", SR_MAX_TREE);
+  SR_CHECK(dtype_ok(d->logit_dtype), "unknown logit dtype %d", (int)d->logit_dtype);
+  SR_CHECK(std::isfinite(d->temperature) && d->temperature > 0.f, "temperature must be finite and > 0");
+  return SR_OK;
+}
+
+size_t sr_tree_accept_workspace(const sr_accept_desc* d) {
+  (void)d;
+  return 0;
+}
+
+sr_status sr_tree_accept(const sr_accept_desc* d, const void* target_logits, const float* child_logit,
+                         const int32_t* tokens, const int32_t* parents, const float* u_acc, const float* u_fin,
+                         int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len, uint8_t* final_kind,
+                         float* min_margin, void* workspace, size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  sr_status st = check_accept_desc(d);
+  if (st != SR_OK) return st;
+  SR_CHECK(target_logits && child_logit && tokens && parents && u_acc && u_fin && out_tokens && out_len && final_kind,
+           "a required pointer is null");
+  SR_CHECK(d->max_depth == 0 || acc_nodes != nullptr, "acc_nodes is null");
+  SR_CHECK(aligned16(target_logits), "target_logits must be 16-byte aligned");
+  return launch_tree_accept(*d, target_logits, child_logit, tokens, parents, u_acc, u_fin, acc_nodes, out_tokens,
+                            out_len, final_kind, min_margin, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ timing hook
+sr_status sr_prof_begin(const char* kernel_substr) {
+  SR_CHECK(kernel_substr != nullptr, "null kernel name");
+  g_prof.on = true;
+  g_prof.pat = kernel_substr;
+  g_prof.used = 0;
+  return SR_OK;
+}
+
+sr_status sr_prof_end(double* total_ms, int32_t* launches) {
+  SR_CHECK(total_ms && launches, "null output");
+  double tot = 0.0;
+  for (int i = 0; i < g_prof.used; ++i) {
+    hipError_t e = hipEventSynchronize(g_prof.stop[i]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, g_prof.start[i], g_prof.stop[i]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = g_prof.used;
+  g_prof.on = false;
+  g_prof.used = 0;
+  return SR_OK;
+}
+
+}  // extern "C"

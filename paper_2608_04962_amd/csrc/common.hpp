@@ -1,0 +1,147 @@
+// Shared device/host helpers of the gfx950 speculative-verification kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "specroll.h"
+
+namespace sr {
+
+typedef uint16_t bf16_t;  // bfloat16 storage (bit pattern)
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+
+// float -> bfloat16 bits, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// Element access for the two storage types.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+  static __device__ __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p, size_t i) { return bf2f(p[i]); }
+  static __device__ __forceinline__ void store(bf16_t* p, size_t i, float v) { p[i] = (bf16_t)f2bf(v); }
+};
+
+__device__ __forceinline__ float warp_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double warp_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double warp_max_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ double warp_min_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ int warp_min_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ int warp_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Topology of one trajectory's tree, held in LDS. Validates parents[0] == -1 and
+// 0 <= parents[c] < c; computes depth, child count and slot index (1-based) of every
+// node. Must be called by the whole block; returns false (uniformly) when invalid.
+template <int MAXT>
+struct TreeLds {
+  int parent[MAXT];
+  int depth[MAXT];
+  int nkids[MAXT];
+  int slot[MAXT];
+  int bad;
+};
+
+template <int MAXT>
+__device__ bool tree_setup(TreeLds<MAXT>& t, const int32_t* parents_b, int T) {
+  const int tid = threadIdx.x;
+  if (tid == 0) t.bad = 0;
+  __syncthreads();
+  for (int c = tid; c < T; c += blockDim.x) {
+    int p = parents_b[c];
+    if ((c == 0 && p != -1) || (c > 0 && (p < 0 || p >= c))) atomicOr(&t.bad, 1);
+    t.parent[c] = p;
+  }
+  __syncthreads();
+  if (t.bad) return false;
+  for (int c = tid; c < T; c += blockDim.x) {
+    int d = 0;
+    for (int p = t.parent[c]; p >= 0; p = t.parent[p]) ++d;  // terminates: parents strictly decrease
+    t.depth[c] = d;
+    int n = 0, s = 0;
+    for (int k = 1; k < T; ++k) {
+      if (t.parent[k] == c) ++n;
+      if (k < c && c > 0 && t.parent[k] == t.parent[c]) ++s;
+    }
+    t.nkids[c] = n;
+    t.slot[c] = (c == 0) ? 0 : s + 1;
+  }
+  __syncthreads();
+  return true;
+}
+
+}  // namespace sr
+
+// ----------------------------------------------------------------------------- host side
+namespace sr {
+
+void set_error(const char* fmt, ...);
+sr_status hip_fail(hipError_t e, const char* what);
+
+// Launch bookkeeping: every kernel launch goes through here so the timing hook can
+// bracket it with events and launch errors are reported uniformly.
+struct LaunchGuard {
+  const char* name;
+  hipStream_t stream;
+  int slot;
+  LaunchGuard(const char* n, hipStream_t s);
+  sr_status done();  // records the closing event (if any) and checks the launch
+};
+
+}  // namespace sr
+
+#define SR_LAUNCH(NAME, KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                 \
+  do {                                                                            \
+    ::sr::LaunchGuard _g((NAME), (STREAM));                                       \
+    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);          \
+    sr_status _st = _g.done();                                                    \
+    if (_st != SR_OK) return _st;                                                 \
+  } while (0)

@@ -1,0 +1,37 @@
+// Launchers implemented in the kernel translation units, called by the C ABI layer.
+#pragma once
+
+#include "common.hpp"
+
+namespace sr {
+
+// ---- proposal (k_heads.hip)
+sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
+                       const void* A, const void* bias, const void* W, float* x, void* n, void* z,
+                       float* logits, hipStream_t s);
+sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const int32_t* parents,
+                            const int32_t* root_token, const float* u_tree, int32_t* tokens, float* child_logit,
+                            int32_t* top_id, float* top_val, hipStream_t s);
+
+// ---- attention (k_attn.hip)
+struct AttnPlan {
+  int R;            // query rows per (trajectory, KV head) = T * Hq / Hkv
+  int Rpad;         // R rounded up to 32
+  int row_groups;   // blocks along the rows
+  int chunk_pages;  // prefix pages per work item
+  int n_chunks;     // work items per (trajectory, KV head), worst case
+  size_t part_o_bytes, part_ml_bytes;
+};
+AttnPlan attn_plan(const sr_attn_desc& d);
+sr_status launch_tree_attn(const sr_attn_desc& d, const AttnPlan& p, const void* q, const void* k_cache,
+                           const void* v_cache, const int32_t* block_table, const int32_t* ctx_len,
+                           const void* k_tree, const void* v_tree, const int32_t* parents, float* out,
+                           float* lse, float* part_o, float* part_ml, hipStream_t s);
+
+// ---- acceptance (k_accept.hip)
+sr_status launch_tree_accept(const sr_accept_desc& d, const void* target_logits, const float* child_logit,
+                             const int32_t* tokens, const int32_t* parents, const float* u_acc,
+                             const float* u_fin, int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len,
+                             uint8_t* final_kind, float* min_margin, hipStream_t s);
+
+}  // namespace sr

@@ -1,0 +1,104 @@
+"""CPU checks of the C ABI: the library loads, exports every function include/specroll.h declares,
+and rejects malformed calls on the host before anything is enqueued (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2608_04962_amd as sr
+from paper_2608_04962_amd import _lib
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "specroll.h")
+
+
+def _declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(sr_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_loads_and_reports_version():
+    assert "gfx950" in sr.version()
+    assert "sr_tree_attn" in sr.kernel_names()
+
+
+def test_every_declared_function_is_exported_and_bound():
+    names = _declared_functions()
+    assert {"sr_heads_propose", "sr_tree_build", "sr_tree_verify_attn", "sr_tree_accept"} <= set(names)
+    h = C.CDLL(_lib.LIB_PATH)
+    for n in names:
+        assert hasattr(h, n), n
+        assert n in _lib.SIGNATURES, f"{n} has no binding"
+
+
+def test_struct_layouts_match_header():
+    # the descriptors are plain int32/float fields in header order
+    assert C.sizeof(_lib.HeadsDesc) == 9 * 4
+    assert C.sizeof(_lib.AttnDesc) == 10 * 4
+    assert C.sizeof(_lib.AcceptDesc) == 6 * 4
+
+
+def _call_heads(desc, **ptrs):
+    args = [ptrs.get(k) for k in ("hidden", "corr", "act", "A", "bias", "W", "parents", "root", "u", "logits", "z",
+                                  "tokens", "cl")]
+    return _lib.lib().sr_heads_propose(C.byref(desc), *args, ptrs.get("ws"), ptrs.get("wsb", 0), None)
+
+
+@pytest.mark.parametrize("field,value", [("B", 0), ("d", 96), ("H", 0), ("T", 0), ("T", 129),
+                                         ("max_children", 8), ("dtype", 7), ("clip_norm", 0.0)])
+def test_heads_descriptor_rejected(field, value):
+    desc = _lib.HeadsDesc(2, 256, 2, 512, 8, 2, _lib.SR_F32, 1.0, 1e-5)
+    setattr(desc, field, value)
+    st = _call_heads(desc)
+    assert st == _lib.SR_ERR_INVALID
+    assert _lib.last_error()
+
+
+def test_heads_null_pointer_and_small_workspace_rejected():
+    desc = _lib.HeadsDesc(2, 256, 2, 512, 8, 2, _lib.SR_F32, 1.0, 1e-5)
+    assert _call_heads(desc) == _lib.SR_ERR_INVALID
+    assert "null" in _lib.last_error()
+    fake = C.c_void_p(1 << 20)   # never dereferenced: the workspace check fails first
+    ptrs = {k: fake for k in ("hidden", "A", "bias", "W", "parents", "root", "u", "tokens", "cl")}
+    st = _call_heads(desc, ws=None, wsb=0, **ptrs)
+    assert st == _lib.SR_ERR_WORKSPACE
+    need = _lib.lib().sr_heads_propose_workspace(C.byref(desc))
+    assert need > 0
+    st = _call_heads(desc, ws=fake, wsb=need - 1, **ptrs)
+    assert st == _lib.SR_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("field,value", [("Hq", 6), ("D", 96), ("block_size", 32), ("max_blocks", 0),
+                                         ("T", 200), ("dtype", 3)])
+def test_attn_descriptor_rejected(field, value):
+    desc = _lib.AttnDesc(2, 8, 4, 4, 64, 16, 10, 20, _lib.SR_F32, 0.125)
+    desc.Hkv = 4
+    if field == "Hq":
+        desc.Hkv = 4
+    setattr(desc, field, value)
+    st = _lib.lib().sr_tree_verify_attn(C.byref(desc), *([None] * 10), None, 0, None)
+    assert st == _lib.SR_ERR_INVALID
+
+
+@pytest.mark.parametrize("field,value", [("V", 12), ("V", 1 << 20), ("temperature", 0.0), ("max_depth", -1),
+                                         ("T", 0)])
+def test_accept_descriptor_rejected(field, value):
+    desc = _lib.AcceptDesc(2, 8, 512, 3, _lib.SR_F32, 1.0)
+    setattr(desc, field, value)
+    st = _lib.lib().sr_tree_accept(C.byref(desc), *([None] * 11), None, 0, None)
+    assert st == _lib.SR_ERR_INVALID
+
+
+def test_workspace_queries_are_consistent():
+    d = _lib.AttnDesc(128, 32, 28, 4, 128, 16, 512, 40000, _lib.SR_BF16, 0.088)
+    ws = _lib.lib().sr_tree_verify_attn_workspace(C.byref(d))
+    assert ws > 0 and ws % 256 == 0
+    d1 = _lib.AttnDesc(2, 8, 4, 2, 64, 16, 10, 20, _lib.SR_F32, 0.125)   # one chunk: no partials
+    assert _lib.lib().sr_tree_verify_attn_workspace(C.byref(d1)) == 0
+    assert _lib.lib().sr_tree_accept_workspace(C.byref(_lib.AcceptDesc(2, 8, 512, 3, 0, 1.0))) == 0
+
+
+def test_prof_hook_host_side():
+    _lib.check(_lib.lib().sr_prof_begin(b"sr_tree_attn"), "begin")
+    assert sr.prof_end() == (0.0, 0)

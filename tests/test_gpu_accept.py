@@ -1,0 +1,173 @@
+"""GPU parity of sr_tree_accept against the float64 oracle (App. B.2), plus exactness statistics of the
+whole GPU proposal + acceptance path (App. B.3, Thm. "Exact target continuation")."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+from scipy import stats
+
+import oracle
+import paper_2608_04962_amd as sr
+import synth
+from helpers import dev_tensor, f64
+
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-6   # decisions closer than this to their threshold may legitimately differ
+
+
+def _gpu_accept(inp, temperature=1.0):
+    res = sr.tree_accept(dev_tensor(inp["target_logits"]), dev_tensor(inp["child_logit"]), dev_tensor(inp["tokens"]),
+                         dev_tensor(inp["parents"]), dev_tensor(inp["u_acc"]), dev_tensor(inp["u_fin"]),
+                         inp["max_depth"], temperature)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in res.items() if v is not None}
+
+
+def _compare(inp, rows=None, temperature=1.0):
+    cfg = inp["cfg"]
+    print(f"[accept] {cfg.name} B={cfg.B} T={cfg.T} V={cfg.V}", flush=True)
+    g = _gpu_accept(inp, temperature)
+    rows = list(range(cfg.B)) if rows is None else [int(r) for r in rows]
+    o = oracle.tree_accept(_Rows(inp["target_logits"], inp["dtype"]), inp["child_logit"], inp["tokens"],
+                           inp["parents"], inp["u_acc"], inp["u_fin"], temperature, inp["max_depth"], rows=rows)
+    exempt = 0
+    for b in rows:
+        same = (np.array_equal(g["acc_nodes"][b], o["acc_nodes"][b])
+                and np.array_equal(g["out_tokens"][b], o["out_tokens"][b])
+                and g["out_len"][b] == o["out_len"][b] and g["final_kind"][b] == o["final_kind"][b])
+        if not same:
+            # only a near-threshold decision may differ
+            assert min(o["min_margin"][b], g["min_margin"][b]) < MARGIN, (b, g["out_tokens"][b], o["out_tokens"][b])
+            exempt += 1
+        assert np.isfinite(g["min_margin"][b])
+    assert exempt <= max(1, len(rows) // 100), exempt
+    return g, o
+
+
+class _Rows:
+    """float64 view of one trajectory's target logits at a time (bounds host memory at full size)."""
+
+    def __init__(self, tl, dt):
+        self.tl, self.dt = tl, dt
+
+    def __getitem__(self, b):
+        return f64(self.tl[b], self.dt)
+
+
+def test_config0_parity():
+    _compare(synth.accept_inputs(synth.CONFIGS[0], seed=0))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_scaled_bf16_parity(seed):
+    cfg = synth.scaled(synth.CONFIGS[2], B=48, V=4096)
+    _compare(synth.accept_inputs(cfg, seed=seed))
+
+
+def test_acceptance_happens_and_walks_deep():
+    # drafts close to the target: most slots accept, walks reach the leaves
+    cfg = synth.scaled(synth.CONFIGS[1], B=64, V=1024, dtype="f32")
+    inp = synth.accept_inputs(cfg, seed=3, target_std=8.0, noise_std=0.05)
+    g, _ = _compare(inp)
+    assert (g["final_kind"] == 1).sum() > 0 and g["out_len"].mean() > 2.0
+
+
+def test_temperature_power_of_two():
+    cfg = synth.scaled(synth.CONFIGS[2], B=16, V=2048, dtype="f32")
+    _compare(synth.accept_inputs(cfg, seed=4), temperature=0.5)
+
+
+def test_single_node_tree_is_plain_sampling():
+    cfg = synth.scaled(synth.CONFIGS[0], T=1, parents=(-1,), B=8)
+    g, o = _compare(synth.accept_inputs(cfg, seed=5))
+    assert (g["out_len"] == 1).all() and (g["final_kind"] == 0).all()
+
+
+def test_invalid_trajectories_are_flagged():
+    cfg = synth.scaled(synth.CONFIGS[0], B=4)
+    inp = synth.accept_inputs(cfg, seed=6)
+    inp["tokens"] = inp["tokens"].copy()
+    inp["tokens"][1, 3] = cfg.V + 3            # token outside the vocabulary
+    inp["tokens"][2, 2] = inp["tokens"][2, 1]  # duplicate sibling tokens
+    inp["parents"] = inp["parents"].copy()
+    inp["parents"][3, 4] = 6                   # not an earlier node
+    g = _gpu_accept(inp)
+    assert list(g["final_kind"][1:]) == [255, 255, 255]
+    assert (g["out_len"][1:] == 0).all() and (g["out_tokens"][1:] == -1).all()
+    assert g["final_kind"][0] in (0, 1)
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2, 3])
+def test_full_size_sampled(cfg_id):
+    cfg = synth.CONFIGS[cfg_id]
+    inp = synth.accept_inputs(cfg, seed=0)
+    rows = np.random.default_rng(cfg_id).choice(cfg.B, size=min(8, cfg.B), replace=False)
+    _compare(inp, rows=rows)
+
+
+def test_deterministic():
+    cfg = synth.scaled(synth.CONFIGS[2], B=32, V=8192)
+    inp = synth.accept_inputs(cfg, seed=7)
+    a = _gpu_accept(inp)
+    b = _gpu_accept(inp)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+# ---------------------------------------------------------------- exactness of the GPU path
+def test_gpu_chi_square_exactness_1e6():
+    """Tree build (sr_tree_build) + acceptance (sr_tree_accept), 1e6 independent trajectories with fresh
+    uniforms: the first committed token must follow p_root and the first two tokens p(x1) p(x2|x1)."""
+    V, H, N = 8, 2, 1_000_000
+    parents = np.array([-1, 0, 0, 0, 1, 1, 2], dtype=np.int32)       # root 3 slots; node 1: 2; node 2: 1
+    T = parents.shape[0]
+    rng = np.random.default_rng(123)
+    head = (rng.standard_normal((H, V)) * 1.2).astype(np.float32)
+    # toy autoregressive target: logits of a node depend on its depth-1 token (the path)
+    base = (rng.standard_normal(V) * 1.5).astype(np.float32)
+    cond = (rng.standard_normal((V, V)) * 1.5).astype(np.float32)
+    dev = "cuda"
+    B = N
+    logits = torch.from_numpy(np.broadcast_to(head, (B, H, V)).copy()).to(dev)
+    par = torch.from_numpy(np.broadcast_to(parents, (B, T)).copy()).to(dev)
+    root = torch.zeros(B, dtype=torch.int32, device=dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    u_tree = torch.rand((B, T), generator=g, device=dev).clamp_(1e-7, 1 - 1e-7)
+    tok, cl = sr.tree_build(logits, par, root, u_tree, max_children=3)
+    # target logits per node: root -> base; depth-1 node with token a -> cond[a]; deeper nodes -> cond[a] too
+    # (the toy target only looks at the first speculative token), so every node's row is a table lookup
+    tokc = tok.long()
+    first_tok = torch.zeros((B, T), dtype=torch.long, device=dev)
+    anc1 = [0, 1, 2, 3, 1, 1, 2]                                        # depth-1 ancestor of each node (0 = root)
+    for c in range(1, T):
+        first_tok[:, c] = tokc[:, anc1[c]]
+    condt = torch.from_numpy(cond).to(dev)
+    tl = condt[first_tok]                                               # [B,T,V]
+    tl[:, 0] = torch.from_numpy(base).to(dev)
+    tl = tl.contiguous()
+    u_acc = torch.rand((B, T), generator=g, device=dev).clamp_(1e-7, 1 - 1e-7)
+    u_fin = torch.rand((B,), generator=g, device=dev).clamp_(1e-7, 1 - 1e-7)
+    res = sr.tree_accept(tl, cl, tok, par, u_acc, u_fin, max_depth=2)
+    out = res["out_tokens"].cpu().numpy()
+    olen = res["out_len"].cpu().numpy()
+    assert (res["final_kind"].cpu().numpy() != 255).all()
+    b64 = base.astype(np.float64)
+    p0 = np.exp(b64 - b64.max()); p0 /= p0.sum()
+    first = np.bincount(out[:, 0], minlength=V)
+    assert stats.chisquare(first, p0 / p0.sum() * N).pvalue > 0.01
+    # second token: where the round committed >= 2 tokens use it, else continue with a fresh draw from p(.|x1)
+    c64 = cond.astype(np.float64)
+    pc = np.exp(c64 - c64.max(1, keepdims=True)); pc /= pc.sum(1, keepdims=True)
+    x1 = out[:, 0]
+    x2 = out[:, 1].copy()
+    need = olen < 2
+    u2 = np.random.default_rng(9).random(need.sum())
+    cdf = np.cumsum(pc[x1[need]], axis=1)
+    x2[need] = (u2[:, None] * cdf[:, -1:] >= cdf).sum(1)
+    joint = np.bincount(x1 * V + x2, minlength=V * V)
+    exp = (p0[:, None] * pc).ravel()
+    exp = exp / exp.sum() * N
+    assert stats.chisquare(joint, exp).pvalue > 0.01

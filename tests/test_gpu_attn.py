@@ -1,0 +1,124 @@
+"""GPU parity of sr_tree_verify_attn against the float64 oracle (App. B.1 Eq. (nodep))."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_04962_amd as sr
+import synth
+from helpers import dev_tensor, f64, row_rel_err, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_gpu(inp):
+    t = {k: dev_tensor(inp[k]) for k in ("q", "k_cache", "v_cache", "k_tree", "v_tree")}
+    out, lse = sr.tree_verify_attn(t["q"], t["k_cache"], t["v_cache"], dev_tensor(inp["block_table"]),
+                                   dev_tensor(inp["ctx_len"]), t["k_tree"], t["v_tree"], dev_tensor(inp["parents"]),
+                                   scale=inp["scale"])
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy()
+
+
+def _oracle(inp, nodes=None):
+    dt = inp["dtype"]
+    return oracle.tree_attention(f64(inp["q"], dt), f64(inp["k_cache"], dt), f64(inp["v_cache"], dt),
+                                 inp["block_table"], inp["ctx_len"], f64(inp["k_tree"], dt), f64(inp["v_tree"], dt),
+                                 inp["parents"], inp["scale"], 16, nodes=nodes)
+
+
+def _check(inp, nodes=None):
+    print(f"[attn] {inp['cfg'].name} B={inp['cfg'].B} T={inp['cfg'].T}", flush=True)
+    out, lse = _run_gpu(inp)
+    ro, rl = _oracle(inp, nodes)
+    tol = tol_for(inp["dtype"])
+    sel = ~np.isnan(ro[..., 0])
+    assert sel.any()
+    err = row_rel_err(out[sel], ro[sel])
+    assert err.max() <= tol, f"max row error {err.max():.3e} > {tol}"
+    # lse: absolute error relative to its magnitude scale
+    lerr = np.abs(lse[sel] - rl[sel]).max()
+    assert lerr <= 10 * tol, lerr
+    assert np.isfinite(out).all()
+    return err.max()
+
+
+def test_config0_all_nodes():
+    _check(synth.attn_inputs(synth.CONFIGS[0], seed=0))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_bf16_multi_chunk_ragged(seed):
+    # contexts straddle the 2048-token chunk size so the split/combine path and ragged tails run
+    cfg = synth.scaled(synth.CONFIGS[2], B=5, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 1, 5000))
+    inp = synth.attn_inputs(cfg, seed=seed)
+    _check(inp)
+
+
+def test_bf16_rows_over_one_block_gqa7():
+    # T*G = 40*7 = 280 > 256 query rows: two row groups
+    cfg = synth.scaled(synth.CONFIGS[2], B=2, T=40, depth=5, ctx=("uniform", 100, 3000))
+    _check(synth.attn_inputs(cfg, seed=3))
+
+
+def test_fp32_d128_and_bf16_d64():
+    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], D=128, Hq=6, Hkv=3), seed=4))
+    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[1], dtype="bf16", B=3, D=64, ctx=("uniform", 20, 300)),
+                             seed=5))
+
+
+def test_empty_prefix_and_single_node_tree():
+    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], ctx=("explicit", (0, 17))), seed=6))
+    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], T=1, parents=(-1,), ctx=("explicit", (0, 2049))),
+                             seed=7))
+    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[2], B=2, T=128, depth=6, Hq=4, Hkv=4,
+                                          ctx=("uniform", 0, 40)), seed=8))
+
+
+def test_invalid_inputs_give_nan_rows_only_for_that_trajectory():
+    cfg = synth.scaled(synth.CONFIGS[2], B=3, T=8, depth=3, Hq=8, Hkv=2, ctx=("uniform", 40, 3000))
+    inp = synth.attn_inputs(cfg, seed=9)
+    inp["block_table"] = inp["block_table"].copy()
+    inp["block_table"][1, 0] = inp["num_blocks"] + 5      # page id out of range
+    inp["ctx_len"] = inp["ctx_len"].copy()
+    inp["ctx_len"][2] = cfg.max_blocks * 16 + 1           # longer than the table
+    out, lse = _run_gpu(inp)
+    assert np.isnan(out[1]).all() and np.isnan(out[2]).all()
+    assert np.isnan(lse[1]).all() and np.isnan(lse[2]).all()
+    assert np.isfinite(out[0]).all()
+    inp2 = synth.attn_inputs(cfg, seed=9)
+    inp2["parents"] = inp2["parents"].copy()
+    inp2["parents"][0, 3] = 5                             # not an earlier node
+    out2, _ = _run_gpu(inp2)
+    assert np.isnan(out2[0]).all() and np.isfinite(out2[1:]).all()
+
+
+def test_deterministic():
+    cfg = synth.scaled(synth.CONFIGS[2], B=4, T=16, depth=4, ctx=("uniform", 1000, 4500))
+    inp = synth.attn_inputs(cfg, seed=10)
+    a, la = _run_gpu(inp)
+    b, lb = _run_gpu(inp)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)
+
+
+def _sample_nodes(cfg, k, seed):
+    rng = np.random.default_rng(seed)
+    bs = rng.choice(cfg.B, size=min(k, cfg.B), replace=False)
+    return [(int(b), int(u)) for b in bs for u in rng.choice(cfg.T, size=min(4, cfg.T), replace=False)]
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2, 3])
+def test_full_size_sampled(cfg_id):
+    cfg = synth.CONFIGS[cfg_id]
+    inp = synth.attn_inputs(cfg, seed=0)
+    _check(inp, nodes=_sample_nodes(cfg, 6, cfg_id))
+
+
+@pytest.mark.parametrize("point", [(256, 8), (4, 96)])
+def test_sweep_points_sampled(point):
+    cfg = synth.sweep_config(*point)
+    inp = synth.attn_inputs(cfg, seed=0)
+    _check(inp, nodes=_sample_nodes(cfg, 4, point[0]))
