@@ -208,7 +208,7 @@ static sr_status check_attn_desc(const sr_attn_desc* d) {
   SR_CHECK(d->max_blocks >= 1 && d->num_blocks >= 1, "max_blocks and num_blocks must be >= 1");
   SR_CHECK((size_t)d->max_blocks * 16 <= (size_t)INT32_MAX / 2, "max_blocks too large");
   SR_CHECK(dtype_ok(d->dtype), "unknown dtype %d", (int)d->dtype);
-  SR_CHECK(std::isfinite(d->scale), "scale must be finite");
+  SR_CHECK(std::isfinite(d->scale) && d->scale > 0.f, "scale must be finite and > 0");
   return SR_OK;
 }
 

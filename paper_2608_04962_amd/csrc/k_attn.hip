@@ -6,10 +6,12 @@
 //
 // Work item = (trajectory b, KV head g, prefix chunk c, row group). The query rows of one
 // work item are the T*G (node, head-in-group) pairs sharing KV head g, so every K/V tile
-// staged in LDS is reused by all of them (GQA sharing). Each wave owns 32 query rows and
-// computes transposed scores S^T = K Q^T on 32x32 MFMA tiles: a lane then holds 16 keys of
-// one query row, so the row max needs one cross-half exchange. P stays in registers and
-// feeds O^T = V^T P^T; V is transposed into LDS when staged. bf16 scores use
+// staged in LDS is reused by all of them (GQA sharing). Each wave owns two 32-row blocks of
+// query rows (every K/V fragment read from LDS feeds two MFMAs) and computes transposed scores
+// S^T = K Q^T on 32x32 MFMA tiles: a lane then holds 16 keys of one query row, so the row max
+// needs one cross-half exchange. P stays in registers and feeds O^T = V^T P^T; V is transposed
+// into LDS when staged. One wave per SIMD leaves room for the accumulators in AGPRs; tile i+1
+// is fetched into registers while tile i is computed from LDS (two LDS stages). bf16 scores use
 // v_mfma_f32_32x32x16_bf16; the probability-weighted V sum uses v_mfma_f32_32x32x16_f16
 // with P and V in fp16 (bf16 P would cost ~3e-3 relative error at 4k-token contexts).
 // The last chunk of a trajectory also processes the T tree keys under the ancestor mask.
@@ -23,7 +25,8 @@ namespace sr {
 
 constexpr int ATT_KT = 64;             // keys per LDS tile
 constexpr int ATT_NW = 8;              // waves per block
-constexpr int ATT_ROWS = ATT_NW * 32;  // query rows per block
+constexpr int ATT_RB = 1;              // 32-row query blocks per wave
+constexpr int ATT_ROWS = ATT_NW * ATT_RB * 32;  // query rows per block
 constexpr int ATT_CHUNK_PAGES = 128;   // prefix pages per work item (2048 tokens)
 constexpr int ATT_BS = 16;             // tokens per page
 
@@ -59,16 +62,45 @@ template <> struct AttnT<float> {
 // key (within a 32-key subtile) held by register i of a lane in half h of a 32x32 output tile
 __device__ __forceinline__ int tile_row(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
 
+// LDS swizzle of V^T rows: 4-key groups of row d live at group position g ^ vswz(d), which keeps both
+// the transposing writes (rows 4 apart) and the MFMA operand reads (32 consecutive rows) free of bank
+// conflicts.
+__device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 2)) & 15; }
+
+template <typename T, int D>
+struct AttnGeom {
+  static constexpr int E = sizeof(T);                    // element bytes in the cache
+  static constexpr int ROWB = D * E;                     // bytes of one K row
+  static constexpr int NCH = ROWB / 16;                  // 16-byte chunks per K row
+  static constexpr int KTILE = ATT_KT * ROWB;            // bytes of a K tile
+  static constexpr int VE = sizeof(typename AttnT<T>::vt);
+  static constexpr int VROWB = ATT_KT * VE;              // bytes of one V^T row (64 keys)
+  static constexpr int VTILE = D * VROWB;
+  static constexpr int NT = ATT_NW * 64;
+  static constexpr int KVEC = KTILE / 16;                // 16-byte K vectors per tile
+  static constexpr int KVPT = KVEC / NT;                 // per thread
+  static constexpr int VITEMS = (ATT_KT / 4) * (D / 4);  // 4 keys x 4 dims per item
+  static constexpr int VIPT = (VITEMS + NT - 1) / NT;    // per thread (the last round may be partial)
+  static_assert(KVEC % NT == 0 && VITEMS % 64 == 0, "tile staging must split evenly over the block");
+};
+
 template <typename T, int D>
 struct AttnSmem {
-  static constexpr int LDK = D + AttnT<T>::PADK;
-  static constexpr int LDV = ATT_KT + AttnT<T>::PADV;
-  T ks[ATT_KT * LDK];
-  typename AttnT<T>::vt vt[D * LDV];
-  int blk[ATT_CHUNK_PAGES];
+  using G = AttnGeom<T, D>;
+  __attribute__((aligned(16))) unsigned char k[2][G::KTILE];
+  __attribute__((aligned(16))) unsigned char v[2][G::VTILE];
+  long long pgoff[ATT_CHUNK_PAGES];     // byte offset of each page of the chunk (this KV head)
   uint32_t anc[SR_MAX_TREE][SR_MAX_TREE / 32];
   int parent[SR_MAX_TREE];
   int bad;
+};
+
+// registers holding one tile's K and V while the previous tile is being computed
+template <typename T, int D>
+struct TileRegs {
+  using G = AttnGeom<T, D>;
+  u32x4 k[G::KVPT];
+  uint32_t v[G::VIPT][4][G::E];  // per item: 4 keys x (4 dims x E bytes)
 };
 
 template <typename T, int D>
@@ -79,20 +111,18 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
     int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max) {
   using AT = AttnT<T>;
+  using G = AttnGeom<T, D>;
   constexpr int KPL = AT::KPL, KSTEP = 2 * KPL;
-  constexpr int VEC = 16 / sizeof(T);
-  constexpr int LDK = AttnSmem<T, D>::LDK, LDV = AttnSmem<T, D>::LDV;
-  constexpr int NQF = D / KSTEP;      // Q fragments per lane
+  constexpr int NQF = D / KSTEP;      // Q fragments per lane and row block
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
-  constexpr int NT = ATT_NW * 64;
-  constexpr int TILE_VECS = ATT_KT * D / VEC;
-  constexpr int VPT = (TILE_VECS + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) AttnSmem<T, D> sm;
+  constexpr int NT = G::NT;
+  constexpr int RB = ATT_RB;
+  __shared__ AttnSmem<T, D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int c = blockIdx.x / row_groups, rg = blockIdx.x % row_groups;
   const int g = blockIdx.y, b = blockIdx.z;
-  const int G = Hq / Hkv;
+  const int G_ = Hq / Hkv;
   const int Lraw = ctx_len[b];
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
   const int L = ctx_ok ? Lraw : 0;
@@ -109,7 +139,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   for (int p = page0 + tid; p < page1; p += NT) {
     int blk = block_table[(size_t)b * max_blocks + p];
     if (blk < 0 || blk >= num_blocks) { atomicOr(&sm.bad, 1); blk = 0; }
-    sm.blk[p - page0] = blk;
+    sm.pgoff[p - page0] = (((long long)blk * Hkv + g) * ATT_BS) * D * (long long)sizeof(T);
   }
   if (last) {
     for (int i = tid; i < T_; i += NT) {
@@ -129,194 +159,288 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   __syncthreads();
   const bool bad = sm.bad != 0;
 
-  // ---- this wave's query rows: row r <-> (node t = r / G, head g*G + r % G)
-  const int rowbase = rg * ATT_ROWS + wave * 32;
-  const int my_r = rowbase + (lane & 31);
-  const bool row_ok = my_r < R;
-  const int my_t = row_ok ? my_r / G : 0;
-  typename AT::qfrag qf[NQF];
-  {
-    const T* qp = q + (((size_t)b * T_ + my_t) * Hq + g * G + (row_ok ? my_r % G : 0)) * D;
+  // ---- this wave's query rows: row r <-> (node t = r / G, head g*G + r % G); RB blocks of 32
+  const int wrow0 = rg * ATT_ROWS + wave * RB * 32;
+  int my_r[RB], my_t[RB];
+  bool row_ok[RB];
+  typename AT::qfrag qf[RB][NQF];
+  uint32_t my_anc[RB][SR_MAX_TREE / 32];
 #pragma unroll
-    for (int ks = 0; ks < NQF; ++ks) {
-      const int dd = ks * KSTEP + half * KPL;
+  for (int rb = 0; rb < RB; ++rb) {
+    my_r[rb] = wrow0 + rb * 32 + (lane & 31);
+    row_ok[rb] = my_r[rb] < R;
+    my_t[rb] = row_ok[rb] ? my_r[rb] / G_ : 0;
+    const T* qp = q + (((size_t)b * T_ + my_t[rb]) * Hq + g * G_ + (row_ok[rb] ? my_r[rb] % G_ : 0)) * D;
+#pragma unroll
+    for (int kq = 0; kq < NQF; ++kq) {
+      const int dd = kq * KSTEP + half * KPL;
       if constexpr (KPL == 8) {
         u32x4 z = {0, 0, 0, 0};
-        if (row_ok) z = *(const u32x4*)(qp + dd);
-        qf[ks] = z;
+        if (row_ok[rb]) z = *(const u32x4*)(qp + dd);
+        qf[rb][kq] = z;
       } else {
-        qf[ks] = row_ok ? qp[dd] : 0.f;
+        qf[rb][kq] = row_ok[rb] ? qp[dd] : 0.f;
       }
     }
-  }
-  uint32_t my_anc[SR_MAX_TREE / 32] = {0, 0, 0, 0};
-  if (last && !bad && row_ok) {
 #pragma unroll
-    for (int w = 0; w < SR_MAX_TREE / 32; ++w) my_anc[w] = sm.anc[my_t][w];
+    for (int w = 0; w < SR_MAX_TREE / 32; ++w) my_anc[rb][w] = (last && !bad && row_ok[rb]) ? sm.anc[my_t[rb]][w] : 0u;
   }
 
-  f32x16 o[NDT];
+  f32x16 o[RB][NDT];
+  float m_run[RB], l_run[RB];
 #pragma unroll
-  for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
-  float m_run = -INFINITY, l_run = 0.f;
-  const bool wave_active = rowbase < R && !bad;
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int i = 0; i < NDT; ++i) o[rb][i] = (f32x16){};
+    m_run[rb] = -INFINITY;
+    l_run[rb] = 0.f;
+  }
+  const bool wave_active = wrow0 < R && !bad;
 
-  // ---- one K/V tile: keys [t0, t0 + ATT_KT) of the prefix (tree == false) or of the tree
-  auto do_tile = [&](int t0, bool tree) {
-    __syncthreads();
-    // stage K (row-major) and V (transposed) in LDS; keys outside the range are zero
+  // ---- tile schedule: prefix tiles of this chunk, then (last chunk) the tree tiles
+  const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
+  const int n_tiles = bad ? 0 : n_pre + (last ? (T_ + ATT_KT - 1) / ATT_KT : 0);
+
+  // global -> registers for tile i. A key past the range is loaded from the range's last key instead
+  // (so nothing past ctx_len is read and every staged value is finite); its score is masked to -inf,
+  // so its K row never matters and its V row is multiplied by an exact zero.
+  const unsigned char* kc_b = (const unsigned char*)k_cache;
+  const unsigned char* vc_b = (const unsigned char*)v_cache;
+  const unsigned char* kt_b = (const unsigned char*)(k_tree + ((size_t)b * T_ * Hkv + g) * D);
+  const unsigned char* vt_b = (const unsigned char*)(v_tree + ((size_t)b * T_ * Hkv + g) * D);
+  const int tree_rowb = Hkv * G::ROWB;                                  // bytes between tree nodes
+  auto load_tile = [&](const unsigned char* kb, const unsigned char* vb, int t0, int lim, auto off_of,
+                       TileRegs<T, D>& r) {
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int v = tid + i * NT;
-      if (v >= TILE_VECS) break;
-      const int key = v / (D / VEC), col = (v % (D / VEC)) * VEC;
-      const int kidx = t0 + key;
-      u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-      if (!bad) {
-        size_t off = 0;
-        bool ok;
-        if (!tree) {
-          ok = kidx < key1;
-          if (ok) off = (((size_t)sm.blk[(kidx >> 4) - page0] * Hkv + g) * ATT_BS + (kidx & 15)) * D + col;
-          if (ok) { kv = *(const u32x4*)(k_cache + off); vv = *(const u32x4*)(v_cache + off); }
+    for (int j = 0; j < G::KVPT; ++j) {
+      const int vi = tid + j * NT;
+      const int key = vi / G::NCH, ch = vi % G::NCH;
+      r.k[j] = *(const u32x4*)(kb + off_of(min(t0 + key, lim - 1)) + ch * 16);
+    }
+#pragma unroll
+    for (int it = 0; it < G::VIPT; ++it) {
+      const int item = tid + it * NT;
+      if (item >= G::VITEMS) break;                   // uniform per wave
+      const int kg = item / (D / 4), dg = item % (D / 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const unsigned char* src = vb + off_of(min(t0 + kg * 4 + j, lim - 1)) + dg * 4 * G::E;
+        if constexpr (G::E == 2) {
+          const u32x2 z = *(const u32x2*)src;
+          r.v[it][j][0] = z[0];
+          r.v[it][j][1] = z[1];
         } else {
-          ok = kidx < T_;
-          if (ok) off = (((size_t)b * T_ + kidx) * Hkv + g) * D + col;
-          if (ok) { kv = *(const u32x4*)(k_tree + off); vv = *(const u32x4*)(v_tree + off); }
-        }
-      }
-      *(u32x4*)(sm.ks + key * LDK + col) = kv;
-      if constexpr (sizeof(T) == 2) {
+          const u32x4 z = *(const u32x4*)src;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t w = vv[e >> 1];
-          const float f = bf2f((e & 1) ? (w >> 16) : (w & 0xffffu));
-          sm.vt[(col + e) * LDV + key] = (_Float16)f;
+          for (int w = 0; w < 4; ++w) r.v[it][j][w] = z[w];
         }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sm.vt[(col + e) * LDV + key] = __uint_as_float(vv[e]);
       }
     }
-    __syncthreads();
-    if (!wave_active) return;
-    // scores S^T for two 32-key subtiles
-    f32x16 s[2];
+  };
+  auto fetch = [&](int i, TileRegs<T, D>& r) {
+    if (i < n_pre) {
+      load_tile(kc_b, vc_b, key0 + i * ATT_KT, key1,
+                [&](int kidx) -> long long { return sm.pgoff[(kidx >> 4) - page0] + (kidx & 15) * G::ROWB; }, r);
+    } else {
+      load_tile(kt_b, vt_b, (i - n_pre) * ATT_KT, T_, [&](int kidx) -> long long { return (long long)kidx * tree_rowb; },
+                r);
+    }
+  };
+  // registers -> LDS stage (K row-major with chunk swizzle, V transposed with group swizzle)
+  auto stash = [&](int st, const TileRegs<T, D>& r) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      s[kt] = (f32x16){};
+    for (int j = 0; j < G::KVPT; ++j) {
+      const int vi = tid + j * NT;
+      const int key = vi / G::NCH, ch = vi % G::NCH;
+      *(u32x4*)(sm.k[st] + key * G::ROWB + ((ch ^ (key & (G::NCH - 1))) * 16)) = r.k[j];
+    }
 #pragma unroll
-      for (int ks = 0; ks < NQF; ++ks) {
-        const T* kp = sm.ks + (kt * 32 + (lane & 31)) * LDK + ks * KSTEP + half * KPL;
+    for (int it = 0; it < G::VIPT; ++it) {
+      const int item = tid + it * NT;
+      if (item >= G::VITEMS) break;
+      const int kg = item / (D / 4), dg = item % (D / 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = dg * 4 + i;
+        unsigned char* dst = sm.v[st] + d * G::VROWB + ((kg ^ vswz(d)) * 4 * G::VE);
+        if constexpr (G::E == 2) {
+          f16x4 h;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t w = r.v[it][j][i >> 1];
+            h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+          }
+          *(f16x4*)dst = h;
+        } else {
+          f32x4 h;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) h[j] = __uint_as_float(r.v[it][j][i]);
+          *(f32x4*)dst = h;
+        }
+      }
+    }
+  };
+
+  auto compute = [&](int i, int st) {
+    const bool tree = i >= n_pre;
+    const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
+    const unsigned char* ks_ = sm.k[st];
+    const unsigned char* vs_ = sm.v[st];
+    // scores S^T: each K fragment feeds both row blocks
+    f32x16 s[RB][2];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = (f32x16){};
+#pragma unroll
+    for (int kq = 0; kq < NQF; ++kq) {
+      const int e = kq * KSTEP + half * KPL;            // first element this lane supplies
+      const int ch = (e * G::E) / 16;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const int key = kt * 32 + (lane & 31);
+        const unsigned char* p = ks_ + key * G::ROWB + ((ch ^ (key & (G::NCH - 1))) * 16) + (e * G::E) % 16;
         typename AT::qfrag kf;
-        if constexpr (KPL == 8) kf = *(const u32x4*)kp; else kf = *kp;
-        s[kt] = AT::mma_qk(kf, qf[ks], s[kt]);
+        if constexpr (KPL == 8) kf = *(const u32x4*)p; else kf = *(const float*)p;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) s[rb][kt] = AT::mma_qk(kf, qf[rb][kq], s[rb][kt]);
       }
     }
-    // mask, scale to log2 units, running max
-    float mx = -INFINITY;
+    // online softmax per row block; vis holds one bit per key of each 32-key subtile, pre-shifted by
+    // this lane half's row offset
+    typename AT::pfrag pf[RB][2][16 / KPL];
+    const bool full = !tree && t0 + ATT_KT <= key1;      // every key of the tile is visible to every row
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      // ancestor word of this 32-key subtile (t0 is a multiple of 64, so the word index is uniform)
-      const int wi = (t0 >> 5) + kt;
-      const uint32_t aw = wi == 0 ? my_anc[0] : wi == 1 ? my_anc[1] : wi == 2 ? my_anc[2] : my_anc[3];
+    for (int rb = 0; rb < RB; ++rb) {
+      uint32_t vis[2];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int kidx = t0 + kt * 32 + tile_row(i, half);
-        bool ok;
-        if (!tree) ok = kidx < key1;
-        else ok = kidx < T_ && ((aw >> (kidx & 31)) & 1u);
-        const float v = ok ? s[kt][i] * scale_log2 : -INFINITY;
-        s[kt][i] = v;
-        mx = fmaxf(mx, v);
-      }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(s[kt][i] - m_use);
-        s[kt][i] = p;
-        psum += p;
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) o[dt] *= alpha;
-    // O^T += V^T P^T; MFMA slot e of step st in half h carries key tile_row(st*KPL + e, h)
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int st = 0; st < 16 / KPL; ++st) {
-        typename AT::pfrag pf;
-        if constexpr (KPL == 8) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s[kt][st * 8 + e];
+      for (int kt = 0; kt < 2; ++kt) {
+        const int kb = t0 + kt * 32;
+        uint32_t v;
+        if (tree) {
+          const int wi = kb >> 5;
+          v = wi == 0 ? my_anc[rb][0] : wi == 1 ? my_anc[rb][1] : wi == 2 ? my_anc[rb][2] : my_anc[rb][3];
         } else {
-          pf = s[kt][st];
+          const int nv = key1 - kb;
+          v = nv >= 32 ? 0xffffffffu : (nv <= 0 ? 0u : ((1u << nv) - 1u));
         }
+        vis[kt] = v >> (4 * half);
+      }
+      if (!full) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const bool ok = (vis[kt] >> (8 * (r >> 2) + (r & 3))) & 1u;
+            s[rb][kt][r] = ok ? s[rb][kt][r] : -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[rb][kt][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // the reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
+      // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled
+      const float tmax = mx * scale_log2;
+      const float m_new = (tmax > m_run[rb] + 8.f) ? tmax : m_run[rb];
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run[rb] - m_use);
+      float psum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][r], scale_log2, -m_use));
+          psum += p;
+          if constexpr (KPL == 8) pf[rb][kt][r >> 3][r & 7] = (_Float16)p;
+          else pf[rb][kt][r] = p;
+        }
+      l_run[rb] = l_run[rb] * alpha + psum;
+      m_run[rb] = m_new;
+      if (__ballot(alpha != 1.f) != 0) {      // rescale only when some row's running max moved
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) o[rb][dt] *= alpha;
+      }
+    }
+    // O^T += V^T P^T; each V fragment feeds both row blocks
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int kq = 0; kq < 16 / KPL; ++kq) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          const typename AT::vt* vp = sm.vt + (dt * 32 + (lane & 31)) * LDV + kt * 32;
+          const int d = dt * 32 + (lane & 31);
+          const unsigned char* vrow = vs_ + d * G::VROWB;
+          const int sw = vswz(d);
           typename AT::pfrag vf;
           if constexpr (KPL == 8) {
-            const int k0 = tile_row(st * 8, half);        // 4 consecutive keys
-            const int k1 = tile_row(st * 8 + 4, half);    // the next 4 consecutive keys
-            const f16x4 lo = *(const f16x4*)(vp + k0);
-            const f16x4 hi = *(const f16x4*)(vp + k1);
+            const int g0 = (kt * 32 + tile_row(kq * 8, half)) >> 2;      // 4 consecutive keys
+            const f16x4 lo = *(const f16x4*)(vrow + ((g0 ^ sw) * 8));
+            const f16x4 hi = *(const f16x4*)(vrow + (((g0 + 2) ^ sw) * 8));
             vf = (f16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
           } else {
-            vf = vp[tile_row(st, half)];
+            const int key = kt * 32 + tile_row(kq, half);
+            vf = *(const float*)(vrow + (((key >> 2) ^ sw) * 16) + (key & 3) * 4);
           }
-          o[dt] = AT::mma_pv(vf, pf, o[dt]);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) o[rb][dt] = AT::mma_pv(vf, pf[rb][kt][kq], o[rb][dt]);
         }
       }
   };
 
-  for (int t0 = key0; t0 < key1; t0 += ATT_KT) do_tile(t0, false);
-  if (last)
-    for (int t0 = 0; t0 < T_; t0 += ATT_KT) do_tile(t0, true);
+  // ---- software pipeline: tile i+1 is in flight (registers) while tile i is computed from LDS
+  if (n_tiles > 0) {
+    TileRegs<T, D> regs;
+    fetch(0, regs);
+    stash(0, regs);
+    __syncthreads();
+    for (int i = 0; i < n_tiles; ++i) {
+      const int st = i & 1;
+      const bool more = i + 1 < n_tiles;
+      if (more) fetch(i + 1, regs);
+      if (wave_active) compute(i, st);
+      if (more) stash(st ^ 1, regs);
+      __syncthreads();
+    }
+  }
 
   // ---- write the normalised result (single chunk) or a partial (m, l, O/l)
-  if (rowbase >= R) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float qnan = __uint_as_float(0x7fc00000u);
-  if (!row_ok) return;
-  if (n_chunks == 1) {
-    const int h = g * G + my_r % G;
-    float* op = out + (((size_t)b * T_ + my_t) * Hq + h) * D;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+  for (int rb = 0; rb < RB; ++rb) {
+    const float l_tot = l_run[rb] + __shfl_xor(l_run[rb], 32, 64);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    if (!row_ok[rb]) continue;
+    if (n_chunks == 1) {
+      const int h = g * G_ + my_r[rb] % G_;
+      float* op = out + (((size_t)b * T_ + my_t[rb]) * Hq + h) * D;
 #pragma unroll
-      for (int i = 0; i < 16; i += 4) {
-        f32x4 v;
+      for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = bad ? qnan : o[dt][i + e] * inv;
-        *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
+        for (int i = 0; i < 16; i += 4) {
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = bad ? qnan : o[rb][dt][i + e] * inv;
+          *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
+        }
+      if (lse != nullptr && half == 0)
+        lse[((size_t)b * T_ + my_t[rb]) * Hq + h] = bad ? qnan : (m_run[rb] + log2f(l_tot)) * kLn2;
+    } else {
+      const size_t pr = (((size_t)b * Hkv + g) * n_chunks_max + c) * Rpad + my_r[rb];
+      float* op = part_o + pr * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; i += 4) {
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = o[rb][dt][i + e] * inv;
+          *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
+        }
+      if (half == 0) {
+        part_ml[pr * 2 + 0] = bad ? qnan : m_run[rb];
+        part_ml[pr * 2 + 1] = bad ? qnan : l_tot;
       }
-    if (lse != nullptr && half == 0)
-      lse[((size_t)b * T_ + my_t) * Hq + h] = bad ? qnan : (m_run + log2f(l_tot)) * kLn2;
-  } else {
-    const size_t pr = (((size_t)b * Hkv + g) * n_chunks_max + c) * Rpad + my_r;
-    float* op = part_o + pr * D;
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 16; i += 4) {
-        f32x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = o[dt][i + e] * inv;
-        *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
-      }
-    if (half == 0) {
-      part_ml[pr * 2 + 0] = bad ? qnan : m_run;
-      part_ml[pr * 2 + 1] = bad ? qnan : l_tot;
     }
   }
 }
