@@ -79,7 +79,7 @@ static bool dtype_ok(sr_dtype t) { return t == SR_F32 || t == SR_BF16; }
   } while (0)
 
 struct HeadsLayout {
-  size_t x, n, z, logits, top_id, top_val, total;
+  size_t x, n, z, logits, top_id, top_val, gmax, need, total;
 };
 static HeadsLayout heads_layout(const sr_heads_desc& d, bool need_z, bool need_logits) {
   HeadsLayout L;
@@ -91,6 +91,8 @@ static HeadsLayout heads_layout(const sr_heads_desc& d, bool need_z, bool need_l
   L.logits = off; if (need_logits) off = align_up(off + B * H * V * 4);
   L.top_id = off; off = align_up(off + B * H * M * 4);
   L.top_val = off; off = align_up(off + B * H * M * 4);
+  L.gmax = off; off = align_up(off + group_max_count(d) * 4);
+  L.need = off; off = align_up(off + B * H * 4);
   L.total = off;
   return L;
 }
@@ -142,7 +144,8 @@ const char* sr_last_error(void) { return g_err.c_str(); }
 const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
 
 const char* sr_kernel_names(void) {
-  return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_topm;sr_tree_build;sr_tree_attn;sr_attn_combine;sr_tree_accept";
+  return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_tree_attn;"
+         "sr_attn_combine;sr_tree_accept";
 }
 
 // ------------------------------------------------------------------ proposal
@@ -170,16 +173,24 @@ sr_status sr_heads_propose(const sr_heads_desc* d, const void* hidden, const flo
   void* zz = z ? z : (void*)(ws + L.z);
   float* lg = logits ? logits : (float*)(ws + L.logits);
   hipStream_t s = (hipStream_t)stream;
-  st = launch_heads(*d, hidden, corr, corr_active, A, bias, W, x, n, zz, lg, s);
+  float* gmax = (float*)(ws + L.gmax);
+  st = launch_heads(*d, hidden, corr, corr_active, A, bias, W, x, n, zz, lg, gmax, s);
   if (st != SR_OK) return st;
-  return launch_tree_build(*d, lg, parents, root_token, u_tree, tokens, child_logit, (int32_t*)(ws + L.top_id),
-                           (float*)(ws + L.top_val), s);
+  return launch_tree_build(*d, lg, gmax, (int32_t*)(ws + L.need), parents, root_token, u_tree, tokens, child_logit,
+                           (int32_t*)(ws + L.top_id), (float*)(ws + L.top_val), s);
+}
+
+static size_t tree_ws_parts(const sr_heads_desc& d, size_t* top, size_t* gm, size_t* need) {
+  *top = align_up((size_t)d.B * d.H * d.max_children * 4);
+  *gm = align_up(group_max_count(d) * 4);
+  *need = align_up((size_t)d.B * d.H * 4);
+  return 2 * *top + *gm + *need;
 }
 
 size_t sr_tree_build_workspace(const sr_heads_desc* d) {
   if (check_heads_desc(d, true) != SR_OK) return 0;
-  const size_t n = (size_t)d->B * d->H * d->max_children * 4;
-  return 2 * align_up(n);
+  size_t a, b, c;
+  return tree_ws_parts(*d, &a, &b, &c);
 }
 
 sr_status sr_tree_build(const sr_heads_desc* d, const float* logits, const int32_t* parents,
@@ -188,12 +199,16 @@ sr_status sr_tree_build(const sr_heads_desc* d, const float* logits, const int32
   sr_status st = check_heads_desc(d, true);
   if (st != SR_OK) return st;
   SR_CHECK(logits && parents && root_token && u_tree && tokens && child_logit, "a required pointer is null");
-  const size_t n = align_up((size_t)d->B * d->H * d->max_children * 4);
-  st = check_ws(workspace, workspace_bytes, 2 * n);
+  size_t top, gm, need;
+  st = check_ws(workspace, workspace_bytes, tree_ws_parts(*d, &top, &gm, &need));
   if (st != SR_OK) return st;
   char* ws = (char*)workspace;
-  return launch_tree_build(*d, logits, parents, root_token, u_tree, tokens, child_logit, (int32_t*)ws,
-                           (float*)(ws + n), (hipStream_t)stream);
+  float* gmax = (float*)(ws + 2 * top);
+  hipStream_t s = (hipStream_t)stream;
+  st = launch_group_max(*d, logits, gmax, s);
+  if (st != SR_OK) return st;
+  return launch_tree_build(*d, logits, gmax, (int32_t*)(ws + 2 * top + gm), parents, root_token, u_tree, tokens,
+                           child_logit, (int32_t*)ws, (float*)(ws + top), s);
 }
 
 // ------------------------------------------------------------------ attention

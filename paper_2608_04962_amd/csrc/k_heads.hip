@@ -83,6 +83,8 @@ template <> struct Mma<float> {
 template <typename T>
 struct EpiHead {
   const T* bias; const float* x; T* z; int d, H;
+  static constexpr bool kGroupMax = false;
+  __device__ __forceinline__ void group_max(int, int, float) const {}
   __device__ __forceinline__ void operator()(int m, int n, float acc) const {
     const int h = n / d, j = n - h * d;
     const float v = acc + Elem<T>::load(bias, n);
@@ -189,6 +191,197 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
     }
 }
 
+// ============================================================================ bf16 GEMM, direct-to-LDS
+// C[m][n] = sum_k A[m][k] * B[n][k] for bf16 operands (both K-contiguous). Tiles stream from global
+// memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring, so STAGES-1 K-steps are
+// in flight while one is multiplied. In LDS a tile row of BK elements is CPR 16-byte chunks; chunk c of
+// row r is stored at position c ^ ((r >> 1) & (CPR - 1)), which keeps the 32x32x16 MFMA operand reads
+// free of bank conflicts. Blocks are mapped so that the M-tiles sharing one N-tile of B run on the same
+// XCD at the same time (B is read from HBM once and hits in that XCD's L2 for the others).
+__device__ __forceinline__ void lds_dma16(const void* gsrc, unsigned char* ldst) {
+  __builtin_amdgcn_global_load_lds((const void*)gsrc, (__attribute__((address_space(3))) void*)ldst, 16, 0, 0);
+}
+
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Epilogue of the vocabulary GEMM: fp32 logits[m][n] plus, per row, the max over each 64-column group
+// (the top-M selection scans only groups whose max can reach the M-th largest value).
+struct EpiLogitsMax {
+  float* out; float* gmax; int N, ngroups;
+  static constexpr bool kGroupMax = true;
+  __device__ __forceinline__ void operator()(int m, int n, float acc) const { out[(size_t)m * N + n] = acc; }
+  __device__ __forceinline__ void group_max(int m, int grp, float v) const {
+    if (grp < ngroups) gmax[(size_t)m * ngroups + grp] = v;   // a tile's last wave may lie past V
+  }
+};
+
+template <int BM, int BN, int BK, int WGM, int WGN, int STAGES, class Epi>
+__global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __restrict__ A,
+                                                            const bf16_t* __restrict__ B, int M, int N, int K,
+                                                            int tiles_m, int tiles_n, Epi epi) {
+  constexpr int NW = WGM * WGN;
+  constexpr int ROWB = BK * 2;                 // bytes per LDS row
+  constexpr int CPR = ROWB / 16;               // 16-byte chunks per row
+  constexpr int RPB = 1024 / ROWB;             // rows per 1 KB DMA block
+  constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
+  constexpr int A_BLK = A_BYTES / 1024, B_BLK = B_BYTES / 1024;
+  constexpr int LPS = (A_BLK + B_BLK) / NW;    // DMA instructions per wave per K-step
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  static_assert((A_BLK + B_BLK) % NW == 0 && A_BLK % NW == 0, "DMA blocks must split evenly over the waves");
+  static_assert(CPR >= 2 && (CPR & (CPR - 1)) == 0 && BK % 16 == 0, "tile");
+  static_assert(STAGES == 4, "the K loop below is unrolled over four LDS stages");
+  // one LDS array per stage, so the compiler can tell the stages' DMA writes apart
+  __shared__ __attribute__((aligned(1024))) unsigned char lds0[A_BYTES + B_BYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds1[A_BYTES + B_BYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds2[A_BYTES + B_BYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds3[A_BYTES + B_BYTES];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  // XCD-aware block -> (mt, nt)
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int mt = local % tiles_m, nt = (local / tiles_m) * 8 + xcd;
+  if (nt >= tiles_n) return;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int nk = K / BK;
+
+  // per-lane DMA source pointers for this wave's blocks (rows past M or N re-read the last row)
+  const unsigned char* srcA[A_BLK / NW];
+  const unsigned char* srcB[B_BLK / NW];
+#pragma unroll
+  for (int j = 0; j < A_BLK / NW; ++j) {
+    const int blk = wave + j * NW;
+    const int r = blk * RPB + lane / CPR, pos = lane % CPR;
+    const int c = pos ^ ((r >> 1) & (CPR - 1));
+    srcA[j] = (const unsigned char*)(A + (size_t)min(m0 + r, M - 1) * K) + c * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < B_BLK / NW; ++j) {
+    const int blk = wave + j * NW;
+    const int r = blk * RPB + lane / CPR, pos = lane % CPR;
+    const int c = pos ^ ((r >> 1) & (CPR - 1));
+    srcB[j] = (const unsigned char*)(B + (size_t)min(n0 + r, N - 1) * K) + c * 16;
+  }
+  auto issue = [&](int ks, unsigned char* dst) {
+    const size_t koff = (size_t)ks * ROWB;
+#pragma unroll
+    for (int j = 0; j < A_BLK / NW; ++j) lds_dma16(srcA[j] + koff, dst + (wave + j * NW) * 1024);
+#pragma unroll
+    for (int j = 0; j < B_BLK / NW; ++j) lds_dma16(srcB[j] + koff, dst + A_BYTES + (wave + j * NW) * 1024);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  // fragment addresses: lane reads row (l%32) of a 32-row group at chunk 2*kk + l/32 (swizzled)
+  const int fr = lane & 31, fh = lane >> 5;
+  auto mma_step = [&](const unsigned char* As) {
+    const unsigned char* Bs = As + A_BYTES;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int c = 2 * kk + fh;
+      u32x4 fa[TM], fb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WTM + i * 32 + fr;
+        fa[i] = *(const u32x4*)(As + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn * WTN + j * 32 + fr;
+        fb[j] = *(const u32x4*)(Bs + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[i]),
+                                                              __builtin_bit_cast(bf16x8, fb[j]), acc[i][j], 0, 0, 0);
+    }
+  };
+  // one K-step: wait for this stage's DMA (the next two steps' may stay in flight), make it visible to
+  // the block, refill the stage consumed one step ago, multiply
+  auto step = [&](int ks, unsigned char* cur, unsigned char* refill) {
+    const int ahead = min(2, nk - 1 - ks);
+    if (ahead >= 2) wait_vmcnt<2 * LPS>();
+    else if (ahead == 1) wait_vmcnt<LPS>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (ks + 3 < nk) issue(ks + 3, refill);
+    mma_step(cur);
+  };
+  if (0 < nk) issue(0, lds0);
+  if (1 < nk) issue(1, lds1);
+  if (2 < nk) issue(2, lds2);
+  for (int ks = 0; ks < nk; ks += 4) {
+    step(ks, lds0, lds3);
+    if (ks + 1 < nk) step(ks + 1, lds1, lds0);
+    if (ks + 2 < nk) step(ks + 2, lds2, lds1);
+    if (ks + 3 < nk) step(ks + 3, lds3, lds2);
+  }
+
+  // epilogue: element stores (lane column l%32, register r -> row 8*(r/4) + 4*(l/32) + r%4)
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WTN + j * 32 + fr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
+        if (m < M && n < N) epi(m, n, acc[i][j][r]);
+      }
+    }
+  if constexpr (Epi::kGroupMax) {
+    static_assert(WTN == 64 && TM * 16 == 64, "group max assumes 64 columns and 64 row slots per lane");
+    // row max over the wave's 64 columns: fold the two 32-column tiles, then reduce across the 32 lanes of
+    // each half by recursive halving (after 5 exchanges a lane owns the maxima of 2 of its 64 row slots)
+    float v[64];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float a = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int n = n0 + wn * WTN + j * 32 + fr;
+          a = fmaxf(a, n < N ? acc[i][j][r] : -INFINITY);
+        }
+        v[i * 16 + r] = a;
+      }
+#pragma unroll
+    for (int step = 0; step < 5; ++step) {
+      const int half_n = 32 >> step;           // values kept after this step
+      const int off = 16 >> step;              // lane distance of the exchange
+      const bool upper = (fr & off) != 0;
+#pragma unroll
+      for (int q = 0; q < half_n; ++q) {
+        const float keep = upper ? v[q + half_n] : v[q];
+        const float send = upper ? v[q] : v[q + half_n];
+        const float recv = __shfl_xor(send, off, 64);
+        v[q] = fmaxf(keep, recv);
+      }
+    }
+    // this lane owns slots s0 and s0 + 1, s0 = sum over exchanged bits
+    const int s0 = ((fr >> 4) & 1) * 32 + ((fr >> 3) & 1) * 16 + ((fr >> 2) & 1) * 8 + ((fr >> 1) & 1) * 4 +
+                   (fr & 1) * 2;
+    const int grp = (n0 + wn * WTN) / 64;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int slot = s0 + e, i = slot >> 4, r = slot & 15;
+      const int m = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
+      if (m < M) epi.group_max(m, grp, v[e]);
+    }
+  }
+}
+
 // ============================================================================ top-M per row
 // Exact selection of the M largest entries of each fp32 row, ordered by (value desc, id asc),
 // by a three-digit radix select on order-preserving keys followed by an id-ordered tie pass.
@@ -232,46 +425,46 @@ __device__ int block_prefix_excl(int v, int* sh, int* total) {
   return incl - v;
 }
 
-__global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logits, int V, int M,
-                                                  int32_t* __restrict__ top_id, float* __restrict__ top_val) {
-  __shared__ int hist[TOPM_BINS];
-  __shared__ int scan[TOPM_NT];
-  __shared__ uint32_t s_prefix, s_pmask;
-  __shared__ int s_rem, s_cnt_eq, s_n;
-  __shared__ uint32_t ck[SR_MAX_TREE];
-  __shared__ int cid[SR_MAX_TREE];
+// Radix select over n order-preserving keys: after it, st.prefix is the key K* of the k-th largest
+// element, st.rem the number of elements equal to K* that belong to the top k, st.cnt_eq how many equal
+// K* in total. Called by the whole block.
+struct RadixState {
+  uint32_t prefix, pmask;
+  int rem, cnt_eq;
+};
+template <class KeyAt>
+__device__ void radix_kth(KeyAt key_at, int n, int k, int* hist, int* scan, RadixState& st) {
   const int tid = threadIdx.x;
-  const float* row = logits + (size_t)blockIdx.x * V;
-  if (tid == 0) { s_prefix = 0; s_pmask = 0; s_rem = M; s_n = 0; }
+  if (tid == 0) { st.prefix = 0; st.pmask = 0; st.rem = k; st.cnt_eq = 0; }
   const int shifts[3] = {21, 10, 0};
   const int bits[3] = {11, 11, 10};
   for (int pass = 0; pass < 3; ++pass) {
     for (int i = tid; i < TOPM_BINS; i += TOPM_NT) hist[i] = 0;
     __syncthreads();
-    const uint32_t prefix = s_prefix, pmask = s_pmask;
+    const uint32_t prefix = st.prefix, pmask = st.pmask;
     const int sh = shifts[pass];
     const uint32_t dmask = (1u << bits[pass]) - 1u;
-    for (int i = tid; i < V; i += TOPM_NT) {
-      uint32_t k = fkey(row[i]);
-      if ((k & pmask) == prefix) atomicAdd(&hist[(k >> sh) & dmask], 1);
+    for (int i = tid; i < n; i += TOPM_NT) {
+      const uint32_t kk = key_at(i);
+      if ((kk & pmask) == prefix) atomicAdd(&hist[(kk >> sh) & dmask], 1);
     }
     __syncthreads();
-    // thread t owns bins [4t, 4t+4); find the bin holding rank s_rem counted from the top
-    const int nb = (1 << bits[pass]) / TOPM_NT;    // 4 or 2
+    // thread t owns bins [nb*t, nb*t + nb); find the bin holding rank st.rem counted from the top
+    const int nb = (1 << bits[pass]) / TOPM_NT;
     int local = 0;
     for (int j = 0; j < nb; ++j) local += hist[tid * nb + j];
     const int above = block_suffix_excl(local, scan);
-    const int rem = s_rem;
+    const int rem = st.rem;
     __syncthreads();
     if (above < rem && rem <= above + local) {
       int a = above;
       for (int j = nb - 1; j >= 0; --j) {
-        int c = hist[tid * nb + j];
+        const int c = hist[tid * nb + j];
         if (rem <= a + c) {
-          s_prefix = prefix | ((uint32_t)(tid * nb + j) << sh);
-          s_pmask = pmask | (dmask << sh);
-          s_rem = rem - a;
-          s_cnt_eq = c;
+          st.prefix = prefix | ((uint32_t)(tid * nb + j) << sh);
+          st.pmask = pmask | (dmask << sh);
+          st.rem = rem - a;
+          st.cnt_eq = c;
           break;
         }
         a += c;
@@ -279,8 +472,27 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logi
     }
     __syncthreads();
   }
-  const uint32_t kstar = s_prefix;
-  const int need_eq = s_rem, cnt_eq = s_cnt_eq;
+}
+
+// Exact top-M of a whole row (radix select + id-ordered tie pass). Used directly by the tree build on
+// caller logits, and as the fallback of the grouped selection; ``need`` (optional) restricts the work to
+// rows whose flag is set.
+__global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logits, int V, int M,
+                                                  int32_t* __restrict__ top_id, float* __restrict__ top_val,
+                                                  const int* __restrict__ need) {
+  if (need != nullptr && need[blockIdx.x] == 0) return;
+  __shared__ int hist[TOPM_BINS];
+  __shared__ int scan[TOPM_NT];
+  __shared__ RadixState st;
+  __shared__ int s_n;
+  __shared__ uint32_t ck[SR_MAX_TREE];
+  __shared__ int cid[SR_MAX_TREE];
+  const int tid = threadIdx.x;
+  const float* row = logits + (size_t)blockIdx.x * V;
+  if (tid == 0) s_n = 0;
+  radix_kth([&](int i) { return fkey(row[i]); }, V, M, hist, scan, st);
+  const uint32_t kstar = st.prefix;
+  const int need_eq = st.rem, cnt_eq = st.cnt_eq;
   if (cnt_eq == need_eq) {
     for (int i = tid; i < V; i += TOPM_NT) {
       uint32_t k = fkey(row[i]);
@@ -314,6 +526,74 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logi
     for (int j = 0; j < M; ++j) rank += (ck[j] > k) || (ck[j] == k && cid[j] < id);
     top_id[(size_t)blockIdx.x * M + rank] = id;
     top_val[(size_t)blockIdx.x * M + rank] = row[id];
+  }
+}
+
+// Max of every 64-column group of each row (for logits that did not come from the vocabulary GEMM).
+__global__ __launch_bounds__(256) void k_group_max(const float* __restrict__ logits, int V, int ngroups,
+                                                   float* __restrict__ gmax) {
+  const int row = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = blockIdx.x * 4 + wave;
+  if (g >= ngroups) return;
+  const int i = g * 64 + lane;
+  float v = i < V ? logits[(size_t)row * V + i] : -INFINITY;
+  v = warp_max(v);
+  if (lane == 0) gmax[(size_t)row * ngroups + g] = v;
+}
+
+// Exact top-M of each row using its 64-column group maxima: tau = the M-th largest group max is a lower
+// bound of the M-th largest value (the top M groups each hold an element >= tau), so every top-M element
+// lies in a group whose max is >= tau and is itself >= tau. Only those groups are read. If more than
+// TOPM_CAP elements qualify (heavy ties), the row is flagged for the full selection.
+constexpr int TOPM_MAXG = 4096;     // V <= 262144
+constexpr int TOPM_CAP = 2048;
+__global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restrict__ logits,
+                                                          const float* __restrict__ gmax, int V, int ngroups, int M,
+                                                          int32_t* __restrict__ top_id, float* __restrict__ top_val,
+                                                          int* __restrict__ need_full) {
+  __shared__ uint32_t gk[TOPM_MAXG];
+  __shared__ int glist[TOPM_MAXG];
+  __shared__ int hist[TOPM_BINS];
+  __shared__ int scan[TOPM_NT];
+  __shared__ RadixState st;
+  __shared__ int s_ng, s_n;
+  __shared__ uint32_t ck[TOPM_CAP];
+  __shared__ int cid[TOPM_CAP];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = blockIdx.x;
+  const float* lrow = logits + (size_t)row * V;
+  for (int g = tid; g < ngroups; g += TOPM_NT) gk[g] = fkey(gmax[(size_t)row * ngroups + g]);
+  if (tid == 0) { s_ng = 0; s_n = 0; }
+  __syncthreads();
+  radix_kth([&](int i) { return gk[i]; }, ngroups, M, hist, scan, st);
+  const uint32_t tau = st.prefix;
+  for (int g = tid; g < ngroups; g += TOPM_NT)
+    if (gk[g] >= tau) glist[atomicAdd(&s_ng, 1)] = g;
+  __syncthreads();
+  const int ng = s_ng;
+  for (int q = wave; q < ng; q += TOPM_NT / 64) {
+    const int i = glist[q] * 64 + lane;
+    if (i < V) {
+      const uint32_t k = fkey(lrow[i]);
+      if (k >= tau) {
+        const int p = atomicAdd(&s_n, 1);
+        if (p < TOPM_CAP) { ck[p] = k; cid[p] = i; }
+      }
+    }
+  }
+  __syncthreads();
+  const int n = s_n;
+  if (tid == 0) need_full[row] = n > TOPM_CAP ? 1 : 0;
+  if (n > TOPM_CAP) return;
+  for (int t = tid; t < n; t += TOPM_NT) {
+    const uint32_t k = ck[t];
+    const int id = cid[t];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += (ck[j] > k) || (ck[j] == k && cid[j] < id);
+    if (rank < M) {
+      top_id[(size_t)row * M + rank] = id;
+      top_val[(size_t)row * M + rank] = lrow[id];
+    }
   }
 }
 
@@ -385,43 +665,84 @@ __global__ __launch_bounds__(SR_MAX_TREE) void k_tree_build(const int32_t* __res
 template <typename T>
 static sr_status launch_heads_t(const sr_heads_desc& d, const void* hidden, const float* corr,
                                 const uint8_t* active, const void* A, const void* bias, const void* W,
-                                float* x, void* n, void* z, float* logits, hipStream_t s) {
+                                float* x, void* n, void* z, float* logits, float* gmax, hipStream_t s) {
   SR_LAUNCH("sr_clip_ln", (k_clip_ln<T>), dim3(d.B), dim3(256), 0, s, (const T*)hidden, corr, active, d.d,
             d.clip_norm, d.ln_eps, x, (T*)n);
-  {
-    constexpr int BM = 64, BN = 128, BK = (sizeof(T) == 2 ? 64 : 32);
-    EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
-    dim3 grid((d.H * d.d + BN - 1) / BN, (d.B + BM - 1) / BM);
-    SR_LAUNCH("sr_head_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
-              (const T*)A, d.B, d.H * d.d, d.d, epi);
-  }
-  {
-    constexpr int BM = 128, BN = 128, BK = (sizeof(T) == 2 ? 64 : 32);
-    EpiLogits epi{logits, d.V};
-    const int M = d.B * d.H;
-    dim3 grid((d.V + BN - 1) / BN, (M + BM - 1) / BM);
-    SR_LAUNCH("sr_vocab_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiLogits>), grid, dim3(256), 0, s, (const T*)z,
-              (const T*)W, M, d.V, d.d, epi);
+  if constexpr (sizeof(T) == 2) {
+    {
+      constexpr int BM = 128, BN = 64, BK = 32;
+      EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
+      const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
+      dim3 grid(((tn + 7) / 8) * 8 * tm);
+      SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+                (const T*)A, d.B, d.H * d.d, d.d, tm, tn, epi);
+    }
+    {
+      constexpr int BM = 256, BN = 256, BK = 32;
+      const int M = d.B * d.H;
+      EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
+      const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
+      dim3 grid(((tn + 7) / 8) * 8 * tm);
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 4, EpiLogitsMax>), grid, dim3(512), 0, s,
+                (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+    }
+  } else {
+    {
+      constexpr int BM = 64, BN = 128, BK = 32;
+      EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
+      dim3 grid((d.H * d.d + BN - 1) / BN, (d.B + BM - 1) / BM);
+      SR_LAUNCH("sr_head_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+                (const T*)A, d.B, d.H * d.d, d.d, epi);
+    }
+    {
+      constexpr int BM = 128, BN = 128, BK = 32;
+      EpiLogits epi{logits, d.V};
+      const int M = d.B * d.H;
+      dim3 grid((d.V + BN - 1) / BN, (M + BM - 1) / BM);
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiLogits>), grid, dim3(256), 0, s, (const T*)z,
+                (const T*)W, M, d.V, d.d, epi);
+      const int ng = (d.V + 63) / 64;
+      SR_LAUNCH("sr_group_max", k_group_max, dim3((ng + 3) / 4, M), dim3(256), 0, s, logits, d.V, ng, gmax);
+    }
   }
   return SR_OK;
 }
 
 sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
                        const void* A, const void* bias, const void* W, float* x, void* n, void* z,
-                       float* logits, hipStream_t s) {
-  if (d.dtype == SR_BF16) return launch_heads_t<bf16_t>(d, hidden, corr, active, A, bias, W, x, n, z, logits, s);
-  return launch_heads_t<float>(d, hidden, corr, active, A, bias, W, x, n, z, logits, s);
+                       float* logits, float* gmax, hipStream_t s) {
+  if (d.dtype == SR_BF16)
+    return launch_heads_t<bf16_t>(d, hidden, corr, active, A, bias, W, x, n, z, logits, gmax, s);
+  return launch_heads_t<float>(d, hidden, corr, active, A, bias, W, x, n, z, logits, gmax, s);
 }
 
-sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const int32_t* parents,
-                            const int32_t* root_token, const float* u_tree, int32_t* tokens, float* child_logit,
-                            int32_t* top_id, float* top_val, hipStream_t s) {
+sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax, int32_t* need_full,
+                            const int32_t* parents, const int32_t* root_token, const float* u_tree,
+                            int32_t* tokens, float* child_logit, int32_t* top_id, float* top_val, hipStream_t s) {
   const int M = d.max_children;
+  const int rows = d.B * d.H;
   if (M > 0) {
-    SR_LAUNCH("sr_topm", k_topm, dim3(d.B * d.H), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val);
+    const int ng = (d.V + 63) / 64;
+    if (gmax != nullptr && ng <= TOPM_MAXG && M <= ng) {
+      SR_LAUNCH("sr_topm", k_topm_grouped, dim3(rows), dim3(TOPM_NT), 0, s, logits, gmax, d.V, ng, M, top_id,
+                top_val, need_full);
+      SR_LAUNCH("sr_topm_full", k_topm, dim3(rows), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val,
+                (const int*)need_full);
+    } else {
+      SR_LAUNCH("sr_topm_full", k_topm, dim3(rows), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val,
+                (const int*)nullptr);
+    }
   }
   SR_LAUNCH("sr_tree_build", k_tree_build, dim3(d.B), dim3(SR_MAX_TREE), 0, s, top_id, top_val, d.H, M, d.T,
             parents, root_token, u_tree, tokens, child_logit);
+  return SR_OK;
+}
+
+size_t group_max_count(const sr_heads_desc& d) { return (size_t)d.B * d.H * ((d.V + 63) / 64); }
+
+sr_status launch_group_max(const sr_heads_desc& d, const float* logits, float* gmax, hipStream_t s) {
+  const int ng = (d.V + 63) / 64;
+  SR_LAUNCH("sr_group_max", k_group_max, dim3((ng + 3) / 4, d.B * d.H), dim3(256), 0, s, logits, d.V, ng, gmax);
   return SR_OK;
 }
 

@@ -8,10 +8,14 @@ namespace sr {
 // ---- proposal (k_heads.hip)
 sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
                        const void* A, const void* bias, const void* W, float* x, void* n, void* z,
-                       float* logits, hipStream_t s);
-sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const int32_t* parents,
-                            const int32_t* root_token, const float* u_tree, int32_t* tokens, float* child_logit,
-                            int32_t* top_id, float* top_val, hipStream_t s);
+                       float* logits, float* gmax, hipStream_t s);
+// per-row maxima of the 64-column groups of fp32 logits [B*H, V]
+size_t group_max_count(const sr_heads_desc& d);
+sr_status launch_group_max(const sr_heads_desc& d, const float* logits, float* gmax, hipStream_t s);
+// top-M supports + ordered child lists; gmax may be null (then a full selection per row runs)
+sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax, int32_t* need_full,
+                            const int32_t* parents, const int32_t* root_token, const float* u_tree,
+                            int32_t* tokens, float* child_logit, int32_t* top_id, float* top_val, hipStream_t s);
 
 // ---- attention (k_attn.hip)
 struct AttnPlan {
