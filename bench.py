@@ -25,6 +25,11 @@ if ROOT not in sys.path:
 METRIC = "verified tree tokens/s per GPU at 7B shape; tree-attn HBM GB/s % peak"
 HBM_PEAK_GBPS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+CALIB_ELEMS = 1 << 28          # 1 GiB of float32 read and 1 GiB written by the calibration copy
+KERNEL_SOURCE = {"sr_tree_attn": "k_attn.hip", "sr_attn_combine": "k_attn.hip", "sr_vocab_gemm": "k_heads.hip",
+                 "sr_head_gemm": "k_heads.hip", "sr_clip_ln": "k_heads.hip", "sr_group_max": "k_heads.hip",
+                 "sr_topm": "k_heads.hip", "sr_topm_full": "k_heads.hip", "sr_tree_build": "k_heads.hip",
+                 "sr_tree_accept": "k_accept.hip"}
 
 
 def log(msg):
@@ -63,7 +68,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=2, help="trajectories the oracle runs on")
+    ap.add_argument("--cpu-sample", type=int, default=32, help="trajectories the oracle runs on")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run a plain 1 GiB float32 elementwise copy (negation) before the steps, as the "
+                         "reference point that scales the HBM byte counters of a profiler run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -115,6 +123,14 @@ def main():
                             A_["v_tree"], A_["parents"], out=out, lse=lse, workspace=aws)
         sr.tree_accept(C_["target_logits"], C_["child_logit"], C_["tokens"], C_["parents"], C_["u_acc"],
                        C_["u_fin"], md, outputs=outs)
+
+    if args.calib_copy:
+        src = torch.ones(CALIB_ELEMS, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step()
@@ -170,7 +186,7 @@ def main():
                                "4 heads, vocab 151936, one attention layer",
                    "global_batch": B, "tree_nodes": T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-                     "traffic": None, "kernel": dominant, "avg_ms": dom_avg_ms, "launches": dom_n},
+                     "traffic": measured_traffic(dominant), "kernel": dominant, "avg_ms": dom_avg_ms, "launches": dom_n},
         "tree_attn": {"GB/s": attn_gbps, "frac_hbm_peak": attn_gbps / HBM_PEAK_GBPS, "ms": attn_ms},
         "kernels_ms": per_kernel,
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
@@ -179,6 +195,29 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, hin, ain, cin, args.cpu_sample)
     print(json.dumps(res), flush=True)
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of ``kernel`` from the committed profiler record (FETCH_SIZE + WRITE_SIZE, each
+    divided by what the same counter reads for the 1 GiB calibration copy), or None when there is no record
+    or the kernel's source has changed since the counters were taken."""
+    import hashlib
+    rec = os.path.join(ROOT, "profiles", f"traffic_{kernel}_7b_step.txt")
+    src = os.path.join(ROOT, "paper_2608_04962_amd", "csrc", KERNEL_SOURCE.get(kernel, ""))
+    if not (os.path.isfile(rec) and os.path.isfile(src)):
+        return None
+    fields = {}
+    for line in open(rec):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != fields.get("source_sha256"):
+            return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(cfg, hin, ain, cin, k):

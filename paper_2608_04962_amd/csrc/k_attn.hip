@@ -304,6 +304,15 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
         for (int rb = 0; rb < RB; ++rb) s[rb][kt] = AT::mma_qk(kf, qf[rb][kq], s[rb][kt]);
       }
     }
+    // interleave the K fragment reads with the score MFMAs (4 reads ahead, then 2 reads per 2 MFMAs)
+    if constexpr (KPL == 8) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+      for (int q = 0; q < 6; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    }
     // online softmax per row block; vis holds one bit per key of each 32-key subtile, pre-shifted by
     // this lane half's row offset
     typename AT::pfrag pf[RB][2][16 / KPL];
@@ -386,6 +395,15 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
           for (int rb = 0; rb < RB; ++rb) o[rb][dt] = AT::mma_pv(vf, pf[rb][kt][kq], o[rb][dt]);
         }
       }
+    // interleave the V fragment reads with the PV MFMAs (8 reads ahead, then 2 reads per MFMA)
+    if constexpr (KPL == 8) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      for (int q = 0; q < 12; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    }
   };
 
   // ---- software pipeline: tile i+1 is in flight (registers) while tile i is computed from LDS
