@@ -31,6 +31,27 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
   return u >> 16;
 }
 
+// 16 bytes per lane from global memory straight into LDS (global_load_lds_dwordx4): lane l's bytes land at
+// ldst + 16 * l, so one wave instruction fills 1 KB; ldst must be the same for every lane of the wave.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, unsigned char* ldst) {
+  __builtin_amdgcn_global_load_lds((const void*)gsrc, (__attribute__((address_space(3))) void*)ldst, 16, 0, 0);
+}
+
+// The same transfer issued as inline assembly, which the compiler does not track: it then inserts no
+// waits of its own for it, and the caller must wait (s_waitcnt vmcnt) before the bytes are read.
+__device__ __forceinline__ void lds_dma16_manual(const void* gsrc, unsigned char* ldst) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)ldst);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gsrc), "s"(l)
+               : "memory", "m0");
+}
+
+// wait until at most N of this wave's vector memory operations (LDS DMA included) are outstanding
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // Element access for the two storage types.
 template <typename T> struct Elem;
 template <> struct Elem<float> {

@@ -84,15 +84,53 @@ struct AttnGeom {
   static_assert(KVEC % NT == 0 && VITEMS % 64 == 0, "tile staging must split evenly over the block");
 };
 
+// Per-block metadata of one work item: the byte offset of every prefix page of the chunk (this KV
+// head), the tree's parents and ancestor masks (last chunk only) and an input-error flag.
+struct AttnMeta {
+  long long pgoff[ATT_CHUNK_PAGES];
+  uint32_t anc[SR_MAX_TREE][SR_MAX_TREE / 32];
+  int parent[SR_MAX_TREE];
+  int bad;
+};
+
+// Fills AttnMeta for pages [page0, page1) of trajectory b and, for the last chunk, its tree; validates
+// the block table entries and the parent array this block reads. Whole block; returns the error flag.
+template <int D, int E>
+__device__ bool attn_meta(AttnMeta& m, bool ctx_ok, bool last, int page0, int page1, const int32_t* bt_b,
+                          const int32_t* par_b, int T_, int Hkv, int g, int num_blocks) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (tid == 0) m.bad = ctx_ok ? 0 : 1;
+  __syncthreads();
+  for (int p = page0 + tid; p < page1; p += nt) {
+    int blk = bt_b[p];
+    if (blk < 0 || blk >= num_blocks) { atomicOr(&m.bad, 1); blk = 0; }
+    m.pgoff[p - page0] = (((long long)blk * Hkv + g) * ATT_BS) * D * (long long)E;
+  }
+  if (last) {
+    for (int i = tid; i < T_; i += nt) {
+      int p = par_b[i];
+      if ((i == 0 && p != -1) || (i > 0 && (p < 0 || p >= i))) atomicOr(&m.bad, 1);
+      m.parent[i] = p;
+    }
+    __syncthreads();
+    if (!m.bad)
+      for (int i = tid; i < T_; i += nt) {
+        uint32_t a[SR_MAX_TREE / 32] = {0, 0, 0, 0};
+        for (int u = i; u >= 0; u = m.parent[u]) a[u >> 5] |= 1u << (u & 31);
+#pragma unroll
+        for (int w = 0; w < SR_MAX_TREE / 32; ++w) m.anc[i][w] = a[w];
+      }
+  }
+  __syncthreads();
+  return m.bad != 0;
+}
+
 template <typename T, int D>
 struct AttnSmem {
   using G = AttnGeom<T, D>;
   __attribute__((aligned(16))) unsigned char k[2][G::KTILE];
   __attribute__((aligned(16))) unsigned char v[2][G::VTILE];
-  long long pgoff[ATT_CHUNK_PAGES];     // byte offset of each page of the chunk (this KV head)
-  uint32_t anc[SR_MAX_TREE][SR_MAX_TREE / 32];
-  int parent[SR_MAX_TREE];
-  int bad;
+  AttnMeta meta;
 };
 
 // registers holding one tile's K and V while the previous tile is being computed
@@ -133,31 +171,9 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   const int page0 = c * ATT_CHUNK_PAGES, page1 = min(pages, page0 + ATT_CHUNK_PAGES);
   const int key0 = page0 * ATT_BS, key1 = min(L, page1 * ATT_BS);
 
-  // ---- stage page ids and (last chunk) the ancestor masks; validate what this block reads
-  if (tid == 0) sm.bad = ctx_ok ? 0 : 1;
-  __syncthreads();
-  for (int p = page0 + tid; p < page1; p += NT) {
-    int blk = block_table[(size_t)b * max_blocks + p];
-    if (blk < 0 || blk >= num_blocks) { atomicOr(&sm.bad, 1); blk = 0; }
-    sm.pgoff[p - page0] = (((long long)blk * Hkv + g) * ATT_BS) * D * (long long)sizeof(T);
-  }
-  if (last) {
-    for (int i = tid; i < T_; i += NT) {
-      int p = parents[(size_t)b * T_ + i];
-      if ((i == 0 && p != -1) || (i > 0 && (p < 0 || p >= i))) atomicOr(&sm.bad, 1);
-      sm.parent[i] = p;
-    }
-    __syncthreads();
-    if (!sm.bad)
-      for (int i = tid; i < T_; i += NT) {
-        uint32_t m[SR_MAX_TREE / 32] = {0, 0, 0, 0};
-        for (int a = i; a >= 0; a = sm.parent[a]) m[a >> 5] |= 1u << (a & 31);
-#pragma unroll
-        for (int w = 0; w < SR_MAX_TREE / 32; ++w) sm.anc[i][w] = m[w];
-      }
-  }
-  __syncthreads();
-  const bool bad = sm.bad != 0;
+  // ---- stage page offsets and (last chunk) the ancestor masks; validate what this block reads
+  const bool bad = attn_meta<D, sizeof(T)>(sm.meta, ctx_ok, last, page0, page1, block_table + (size_t)b * max_blocks,
+                                           parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
 
   // ---- this wave's query rows: row r <-> (node t = r / G, head g*G + r % G); RB blocks of 32
   const int wrow0 = rg * ATT_ROWS + wave * RB * 32;
@@ -183,7 +199,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
       }
     }
 #pragma unroll
-    for (int w = 0; w < SR_MAX_TREE / 32; ++w) my_anc[rb][w] = (last && !bad && row_ok[rb]) ? sm.anc[my_t[rb]][w] : 0u;
+    for (int w = 0; w < SR_MAX_TREE / 32; ++w) my_anc[rb][w] = (last && !bad && row_ok[rb]) ? sm.meta.anc[my_t[rb]][w] : 0u;
   }
 
   f32x16 o[RB][NDT];
@@ -240,7 +256,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   auto fetch = [&](int i, TileRegs<T, D>& r) {
     if (i < n_pre) {
       load_tile(kc_b, vc_b, key0 + i * ATT_KT, key1,
-                [&](int kidx) -> long long { return sm.pgoff[(kidx >> 4) - page0] + (kidx & 15) * G::ROWB; }, r);
+                [&](int kidx) -> long long { return sm.meta.pgoff[(kidx >> 4) - page0] + (kidx & 15) * G::ROWB; }, r);
     } else {
       load_tile(kt_b, vt_b, (i - n_pre) * ATT_KT, T_, [&](int kidx) -> long long { return (long long)kidx * tree_rowb; },
                 r);
@@ -463,6 +479,307 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   }
 }
 
+// ============================================================================ bf16, direct-to-LDS
+// The bf16 path streams K and V tiles from HBM straight into LDS (global_load_lds_dwordx4) through a
+// three-slot ring: while tile i is finished, tiles i+2 and i+3 are in flight. In LDS, 16-byte chunk c of
+// key row k sits at chunk position c ^ (k mod NCH) for K and c ^ ((k / 4) mod NCH) for V, chosen by the
+// source address each lane loads, which keeps the operand reads free of bank conflicts. Once per tile the
+// block transposes V (bf16 -> fp16) into a two-slot V^T ring whose rows hold the keys in the order the
+// MFMA operand wants them, so a V^T fragment is one 16-byte read. Each wave computes the scores of
+// tile i+1 in the same instruction stream as the exponentials of tile i, so its matrix and vector
+// work overlap. One barrier per tile.
+template <int D>
+struct DmaGeom {
+  static constexpr int ROWB = D * 2;                   // bytes of one K or V row
+  static constexpr int NCH = ROWB / 16;                // 16-byte chunks per row
+  static constexpr int KPB = 1024 / ROWB;              // keys per 1 KB DMA block
+  static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
+  static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
+  static constexpr int BPW = BLK / ATT_NW;             // ... per wave
+  static constexpr int LPT = 2 * BPW;                  // DMA instructions per wave and tile
+  static constexpr int VT_ROWB = ATT_KT * 2;           // bytes of one V^T row (64 keys, fp16)
+  static constexpr int VTILE = D * VT_ROWB;
+  static constexpr int TITEMS = (ATT_KT / 4) * (D / 4);  // transpose items of 4 keys x 4 dims
+  static_assert(BLK % ATT_NW == 0 && TITEMS % 64 == 0 && TITEMS <= ATT_NW * 64, "tile split");
+  static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
+};
+
+// V^T row d: 16-byte slot s holds key groups (4 keys each) g and g + 2 with s = 2*(g/4) + g%2, stored
+// at slot position s ^ vtswz(d); 8 consecutive rows and 8 consecutive even (or odd) rows hit 8 distinct
+// positions, so the fragment reads of 32 rows are conflict-free.
+__device__ __forceinline__ int vtswz(int d) { return (d ^ (d >> 3)) & 7; }
+
+template <int D>
+__device__ __forceinline__ void lds_barrier_after_dma_wait(int ahead) {
+  // make this wave's LDS writes and its DMA for the next tile complete, then meet the block
+  constexpr int L = DmaGeom<D>::LPT;
+  if (ahead > 0) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(L) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int D>
+__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache, const bf16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
+    const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
+    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max) {
+  using G = DmaGeom<D>;
+  constexpr int NQF = D / 16;         // Q fragments per lane
+  constexpr int NDT = D / 32;         // 32-wide output tiles along D
+  // ring slot: K tile, then raw V tile
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[3][2 * G::TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char vtr[2][G::VTILE];
+  __shared__ AttnMeta meta;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int c = blockIdx.x / row_groups, rg = blockIdx.x % row_groups;
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int G_ = Hq / Hkv;
+  const int Lraw = ctx_len[b];
+  const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
+  const int L = ctx_ok ? Lraw : 0;
+  const int pages = (L + ATT_BS - 1) / ATT_BS;
+  const int n_chunks = ctx_ok ? max(1, (pages + ATT_CHUNK_PAGES - 1) / ATT_CHUNK_PAGES) : 1;
+  if (c >= n_chunks) return;
+  const bool last = c == n_chunks - 1;
+  const int page0 = c * ATT_CHUNK_PAGES, page1 = min(pages, page0 + ATT_CHUNK_PAGES);
+  const int key0 = page0 * ATT_BS, key1 = min(L, page1 * ATT_BS);
+
+  const bool bad = attn_meta<D, 2>(meta, ctx_ok, last, page0, page1, block_table + (size_t)b * max_blocks,
+                                   parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
+
+  // ---- this wave's 32 query rows: row r <-> (node t = r / G, head g*G + r % G)
+  const int my_r = rg * ATT_ROWS + wave * 32 + (lane & 31);
+  const bool row_ok = my_r < R;
+  const int my_t = row_ok ? my_r / G_ : 0;
+  u32x4 qf[NQF];
+  {
+    const bf16_t* qp = q + (((size_t)b * T_ + my_t) * Hq + g * G_ + (row_ok ? my_r % G_ : 0)) * D;
+#pragma unroll
+    for (int kq = 0; kq < NQF; ++kq) {
+      u32x4 z = {0, 0, 0, 0};
+      if (row_ok) z = *(const u32x4*)(qp + kq * 16 + half * 8);
+      qf[kq] = z;
+    }
+    // the K/V DMA below is invisible to the compiler's wait counting, so every compiler-tracked load
+    // must have landed before the first transfer is issued
+#pragma unroll
+    for (int kq = 0; kq < NQF; ++kq) asm volatile("" ::"v"(qf[kq]));
+  }
+
+  f32x16 o[NDT];
+#pragma unroll
+  for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
+  float m_run = -INFINITY, l_run = 0.f;
+  const bool wave_active = rg * ATT_ROWS + wave * 32 < R && !bad;
+
+  const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
+  const int n_tiles = bad ? 0 : n_pre + (last ? (T_ + ATT_KT - 1) / ATT_KT : 0);
+
+  const unsigned char* kc_b = (const unsigned char*)k_cache;
+  const unsigned char* vc_b = (const unsigned char*)v_cache;
+  const unsigned char* kt_b = (const unsigned char*)(k_tree + ((size_t)b * T_ * Hkv + g) * D);
+  const unsigned char* vt_b = (const unsigned char*)(v_tree + ((size_t)b * T_ * Hkv + g) * D);
+  const long long tree_rowb = (long long)Hkv * G::ROWB;
+
+  // global -> LDS for tile i. A key past the range is loaded from the range's last key instead (nothing
+  // past ctx_len is read and every staged value is finite); its score is masked to -inf, so its K row
+  // never matters and its V row is multiplied by an exact zero.
+  auto issue = [&](int i, unsigned char* slot) {
+    const bool tree = i >= n_pre;
+    const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
+#pragma unroll
+    for (int j = 0; j < G::BPW; ++j) {
+      const int blk = wave + j * ATT_NW;
+      const int kk = blk * G::KPB + lane / G::NCH, pos = lane % G::NCH;
+      long long off;
+      if (tree) {
+        off = (long long)min(t0 + kk, T_ - 1) * tree_rowb;
+      } else {
+        const int key = min(t0 + kk, key1 - 1);
+        off = meta.pgoff[(key >> 4) - page0] + (key & 15) * G::ROWB;
+      }
+      const unsigned char* kb = (tree ? kt_b : kc_b) + off;
+      const unsigned char* vb = (tree ? vt_b : vc_b) + off;
+      lds_dma16_manual(kb + ((pos ^ (kk & (G::NCH - 1))) * 16), slot + blk * 1024);
+      lds_dma16_manual(vb + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16), slot + G::TILE + blk * 1024);
+    }
+  };
+  // raw V (bf16, [key][d]) -> V^T (fp16); thread = (4-key group kg, 4-dim group dg)
+  auto transpose = [&](const unsigned char* rawv, unsigned char* vt) {
+    if (tid < G::TITEMS) {                      // uniform per wave
+      const int kg = tid & 15, dg = tid >> 4;
+      u32x2 r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int pos = (dg >> 1) ^ (kg & (G::NCH - 1));
+        r[j] = *(const u32x2*)(rawv + (4 * kg + j) * G::ROWB + pos * 16 + (dg & 1) * 8);
+      }
+      const int slot = ((kg >> 2) << 1) | (kg & 1), sub = (kg >> 1) & 1;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = 4 * dg + i;
+        f16x4 h;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t w = r[j][i >> 1];
+          h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+        }
+        *(f16x4*)(vt + d * G::VT_ROWB + ((slot ^ vtswz(d)) * 16) + sub * 8) = h;
+      }
+    }
+  };
+  // scores S^T = K Q^T of the tile in ks
+  auto qk = [&](const unsigned char* ks, f32x16 (&s)[2]) {
+    s[0] = s[1] = (f32x16){};
+#pragma unroll
+    for (int kq = 0; kq < NQF; ++kq) {
+      const int ch = 2 * kq + half;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const int key = kt * 32 + (lane & 31);
+        const u32x4 kf = *(const u32x4*)(ks + key * G::ROWB + ((ch ^ (key & (G::NCH - 1))) * 16));
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf),
+                                                        __builtin_bit_cast(bf16x8, qf[kq]), s[kt], 0, 0, 0);
+      }
+    }
+  };
+  // mask, online softmax and O^T += V^T P^T for tile i (scores s); the next tile's scores (K in nks) are
+  // computed into sn in the same basic block as this tile's exponentials
+  auto finish = [&](int i, f32x16 (&s)[2], const unsigned char* vt, const unsigned char* nks, f32x16 (&sn)[2]) {
+    const bool tree = i >= n_pre;
+    const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
+    const bool full = !tree && t0 + ATT_KT <= key1;
+    if (!full) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const int kb = t0 + kt * 32;
+        uint32_t v;
+        if (tree) {
+          v = (row_ok && last) ? meta.anc[my_t][kb >> 5] : 0u;
+        } else {
+          const int nv = key1 - kb;
+          v = nv >= 32 ? 0xffffffffu : (nv <= 0 ? 0u : ((1u << nv) - 1u));
+        }
+        v >>= 4 * half;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool ok = (v >> (8 * (r >> 2) + (r & 3))) & 1u;
+          s[kt][r] = ok ? s[kt][r] : -INFINITY;
+        }
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    // the reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
+    // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled
+    const float tmax = mx * scale_log2;
+    const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    qk(nks, sn);
+    f16x8 pf[2][2];
+    float psum = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
+        psum += p;
+        pf[kt][r >> 3][r & 7] = (_Float16)p;
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    if (__ballot(alpha != 1.f) != 0) {      // rescale only when some row's running max moved
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) o[dt] *= alpha;
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int kq = 0; kq < 2; ++kq)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const int d = dt * 32 + (lane & 31);
+          const f16x8 vf = *(const f16x8*)(vt + d * G::VT_ROWB + (((4 * kt + 2 * kq + half) ^ vtswz(d)) * 16));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[kt][kq], o[dt], 0, 0, 0);
+        }
+  };
+
+  // ---- pipeline. step(i): wait for tile i+1, refill the slot tile i used with tile i+3, transpose
+  // V of tile i+1, then finish tile i while computing the scores of tile i+1 (slot of tile i: si).
+  f32x16 sa[2], sb[2];
+  auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
+    const int sn_ = si == 2 ? 0 : si + 1;
+    lds_barrier_after_dma_wait<D>(i + 2 < n_tiles ? 1 : 0);
+    if (i + 3 < n_tiles) issue(i + 3, ring[si]);
+    if (i + 1 < n_tiles) transpose(ring[sn_] + G::TILE, vtr[(i + 1) & 1]);
+    // after the last tile the next scores come from a slot no DMA is writing and are discarded
+    if (wave_active) finish(i, s, vtr[i & 1], ring[sn_], sn);
+  };
+  if (n_tiles > 0) {
+    issue(0, ring[0]);
+    if (n_tiles > 1) issue(1, ring[1]);
+    if (n_tiles > 2) issue(2, ring[2]);
+    if (n_tiles > 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * G::LPT) : "memory");
+    else if (n_tiles > 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(G::LPT) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    transpose(ring[0] + G::TILE, vtr[0]);
+    if (wave_active) qk(ring[0], sa);
+    int si = 0;
+    for (int i = 0; i < n_tiles; i += 2) {
+      step(i, si, sa, sb);
+      si = si == 2 ? 0 : si + 1;
+      if (i + 1 < n_tiles) {
+        step(i + 1, si, sb, sa);
+        si = si == 2 ? 0 : si + 1;
+      }
+    }
+  }
+
+  // ---- write the normalised result (single chunk) or a partial (m, l, O/l)
+  const float qnan = __uint_as_float(0x7fc00000u);
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (!row_ok) return;
+  if (n_chunks == 1) {
+    const int h = g * G_ + my_r % G_;
+    float* op = out + (((size_t)b * T_ + my_t) * Hq + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; i += 4) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = bad ? qnan : o[dt][i + e] * inv;
+        *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
+      }
+    if (lse != nullptr && half == 0)
+      lse[((size_t)b * T_ + my_t) * Hq + h] = bad ? qnan : (m_run + log2f(l_tot)) * kLn2;
+  } else {
+    const size_t pr = (((size_t)b * Hkv + g) * n_chunks_max + c) * Rpad + my_r;
+    float* op = part_o + pr * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; i += 4) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][i + e] * inv;
+        *(f32x4*)(op + dt * 32 + tile_row(i, half)) = v;
+      }
+    if (half == 0) {
+      part_ml[pr * 2 + 0] = bad ? qnan : m_run;
+      part_ml[pr * 2 + 1] = bad ? qnan : l_tot;
+    }
+  }
+}
+
 // Merge the chunk partials of every (trajectory, KV head) that was split.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_combine(const int32_t* __restrict__ ctx_len,
@@ -529,9 +846,15 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
                                hipStream_t s) {
   const float scale_log2 = d.scale * kLog2e;
   dim3 grid(p.n_chunks * p.row_groups, d.Hkv, d.B);
-  SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
-            (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
-            d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks);
+  if constexpr (sizeof(T) == 2) {
+    SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
+              (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks);
+  } else {
+    SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
+              (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks);
+  }
   if (p.n_chunks > 1) {
     constexpr int RPB = 256 / (D / 4);
     dim3 cgrid((p.R + RPB - 1) / RPB, d.Hkv, d.B);

@@ -198,15 +198,6 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
 // row r is stored at position c ^ ((r >> 1) & (CPR - 1)), which keeps the 32x32x16 MFMA operand reads
 // free of bank conflicts. Blocks are mapped so that the M-tiles sharing one N-tile of B run on the same
 // XCD at the same time (B is read from HBM once and hits in that XCD's L2 for the others).
-__device__ __forceinline__ void lds_dma16(const void* gsrc, unsigned char* ldst) {
-  __builtin_amdgcn_global_load_lds((const void*)gsrc, (__attribute__((address_space(3))) void*)ldst, 16, 0, 0);
-}
-
-template <int N> __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
 // Epilogue of the vocabulary GEMM: fp32 logits[m][n] plus, per row, the max over each 64-column group
 // (the top-M selection scans only groups whose max can reach the M-th largest value).
 struct EpiLogitsMax {
