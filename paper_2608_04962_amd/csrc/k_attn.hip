@@ -18,6 +18,8 @@
 // Several chunks of one (b, g) are merged by log-sum-exp in k_attn_combine.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -495,12 +497,11 @@ struct DmaGeom {
   static constexpr int KPB = 1024 / ROWB;              // keys per 1 KB DMA block
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
-  static constexpr int BPW = BLK / ATT_NW;             // ... per wave
-  static constexpr int LPT = 2 * BPW;                  // DMA instructions per wave and tile
   static constexpr int VT_ROWB = ATT_KT * 2;           // bytes of one V^T row (64 keys, fp16)
   static constexpr int VTILE = D * VT_ROWB;
   static constexpr int TITEMS = (ATT_KT / 4) * (D / 4);  // transpose items of 4 keys x 4 dims
   static_assert(BLK % ATT_NW == 0 && TITEMS % 64 == 0 && TITEMS <= ATT_NW * 64, "tile split");
+  static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
 };
 
@@ -509,12 +510,23 @@ struct DmaGeom {
 // positions, so the fragment reads of 32 rows are conflict-free.
 __device__ __forceinline__ int vtswz(int d) { return (d ^ (d >> 3)) & 7; }
 
+// Complete this wave's LDS writes and its DMA for the next tile, then meet the block. A wave that
+// issues DMA (one of npd such waves, each with 2*BLK/npd transfers per tile) may leave the transfers
+// of the tile after that in flight when `ahead`.
 template <int D>
-__device__ __forceinline__ void lds_barrier_after_dma_wait(int ahead) {
-  // make this wave's LDS writes and its DMA for the next tile complete, then meet the block
-  constexpr int L = DmaGeom<D>::LPT;
-  if (ahead > 0) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(L) : "memory");
-  else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+__device__ __forceinline__ void attn_sync(int npd, bool dma_wave, bool ahead) {
+  constexpr int BLK = DmaGeom<D>::BLK;
+  if (!dma_wave || !ahead) {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  } else if (npd == 1) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * BLK) : "memory");
+  } else if (npd == 2) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK) : "memory");
+  } else if (npd == 4) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK / 2) : "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK / 4) : "memory");
+  }
 }
 
 template <int D>
@@ -572,7 +584,16 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
 #pragma unroll
   for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
   float m_run = -INFINITY, l_run = 0.f;
-  const bool wave_active = rg * ATT_ROWS + wave * 32 < R && !bad;
+  // Roles. Without any wave free of query rows, all waves share the DMA and the V transposition. Else
+  // the first row-free wave issues all of the DMA (npd = 1), pacing itself on the memory system, and
+  // the other seven waves transpose V.
+  const int n_act = min(ATT_NW, (R - rg * ATT_ROWS + 31) / 32);
+  const int n_prod = ATT_NW - n_act;
+  const bool wave_active = wave < n_act && !bad;
+  const int npd = n_prod == 0 ? ATT_NW : 1;
+  const bool dma_wave = n_prod == 0 || wave == n_act;
+  const int n_tr = n_prod == 0 ? ATT_NW : ATT_NW - 1;
+  const int tr_rank = (n_prod == 0 || wave < n_act) ? wave : (wave == n_act ? -1 : wave - 1);
 
   const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
   const int n_tiles = bad ? 0 : n_pre + (last ? (T_ + ATT_KT - 1) / ATT_KT : 0);
@@ -586,47 +607,107 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   // global -> LDS for tile i. A key past the range is loaded from the range's last key instead (nothing
   // past ctx_len is read and every staged value is finite); its score is masked to -inf, so its K row
   // never matters and its V row is multiplied by an exact zero.
-  auto issue = [&](int i, unsigned char* slot) {
+  // Source of DMA block blk (KPB keys x 1 KB) of tile i for this lane: the K and V byte offsets.
+  auto block_src = [&](int i, int blk, long long& ko, long long& vo) __attribute__((always_inline)) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));                  // not hoisted out of the tile loop
+    const int kk = blk * G::KPB + ln / G::NCH, pos = ln % G::NCH;
+    long long off;
+    if (tree) {
+      off = (long long)min(t0 + kk, T_ - 1) * tree_rowb;
+    } else {
+      const int key = min(t0 + kk, key1 - 1);
+      off = meta.pgoff[(key >> 4) - page0] + (key & 15) * G::ROWB;
+    }
+    const long long base = tree ? (long long)(kt_b - kc_b) : 0;   // tree rows are addressed from kc_b
+    ko = base + off + ((pos ^ (kk & (G::NCH - 1))) * 16);
+    vo = (tree ? (long long)(vt_b - vc_b) : 0) + off + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16);
+  };
+  // every wave issues its BLK/8 blocks of K and of V (all waves have query rows)
+  auto issue_dist = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < G::BPW; ++j) {
+    for (int j = 0; j < G::BLK / ATT_NW; ++j) {
       const int blk = wave + j * ATT_NW;
-      const int kk = blk * G::KPB + lane / G::NCH, pos = lane % G::NCH;
-      long long off;
-      if (tree) {
-        off = (long long)min(t0 + kk, T_ - 1) * tree_rowb;
-      } else {
-        const int key = min(t0 + kk, key1 - 1);
-        off = meta.pgoff[(key >> 4) - page0] + (key & 15) * G::ROWB;
-      }
-      const unsigned char* kb = (tree ? kt_b : kc_b) + off;
-      const unsigned char* vb = (tree ? vt_b : vc_b) + off;
-      lds_dma16_manual(kb + ((pos ^ (kk & (G::NCH - 1))) * 16), slot + blk * 1024);
-      lds_dma16_manual(vb + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16), slot + G::TILE + blk * 1024);
+      long long ko, vo;
+      block_src(i, blk, ko, vo);
+      lds_dma16_manual(kc_b + ko, slot + blk * 1024);
+      lds_dma16_manual(vc_b + vo, slot + G::TILE + blk * 1024);
     }
   };
-  // raw V (bf16, [key][d]) -> V^T (fp16); thread = (4-key group kg, 4-dim group dg)
-  auto transpose = [&](const unsigned char* rawv, unsigned char* vt) {
-    if (tid < G::TITEMS) {                      // uniform per wave
-      const int kg = tid & 15, dg = tid >> 4;
-      u32x2 r[4];
+  // one producer wave issues the whole tile: for a full prefix tile the four page offsets are read
+  // once and every block's lane offset is a constant; other tiles take the per-lane clamped path
+  auto issue_prod = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
+    const bool tree = i >= n_pre;
+    const int t0 = tree ? 0 : key0 + i * ATT_KT;
+    if (!tree && t0 + ATT_KT <= key1) {
+      const int pg = (t0 >> 4) - page0;
+      long long po[ATT_KT / ATT_BS];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int pos = (dg >> 1) ^ (kg & (G::NCH - 1));
-        r[j] = *(const u32x2*)(rawv + (4 * kg + j) * G::ROWB + pos * 16 + (dg & 1) * 8);
+      for (int p = 0; p < ATT_KT / ATT_BS; ++p) po[p] = meta.pgoff[pg + p];
+      // an opaque copy of the lane id keeps the per-block lane offsets from being hoisted out of the
+      // tile loop (32 of them would stay live in registers)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+#pragma unroll
+      for (int blk = 0; blk < G::BLK; ++blk) {
+        const int kk = blk * G::KPB + ln / G::NCH, pos = ln % G::NCH;
+        const long long row = po[kk >> 4] + (kk & 15) * G::ROWB;
+        lds_dma16_manual(kc_b + row + ((pos ^ (kk & (G::NCH - 1))) * 16), slot + blk * 1024);
+        lds_dma16_manual(vc_b + row + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16), slot + G::TILE + blk * 1024);
+        __builtin_amdgcn_sched_barrier(0);        // keep each address next to its transfer
       }
-      const int slot = ((kg >> 2) << 1) | (kg & 1), sub = (kg >> 1) & 1;
+    } else {
+      for (int blk = 0; blk < G::BLK; ++blk) {
+        long long ko, vo;
+        block_src(i, blk, ko, vo);
+        lds_dma16_manual(kc_b + ko, slot + blk * 1024);
+        lds_dma16_manual(vc_b + vo, slot + G::TILE + blk * 1024);
+      }
+    }
+  };
+  auto issue = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
+    if (n_prod == 0) issue_dist(i, slot);
+    else issue_prod(i, slot);
+  };
+  // raw V (bf16, [key][d]) -> V^T (fp16); item = (4-key group kg, 4-dim group dg), two items per lane
+  // at a time with all their reads issued first
+  auto transpose = [&](const unsigned char* rawv, unsigned char* vt) __attribute__((always_inline)) {
+    if (tr_rank < 0) return;                    // the DMA wave
+    const int stride = n_tr * 64;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
+    for (int it0 = tr_rank * 64 + ln; it0 < G::TITEMS; it0 += 2 * stride) {   // uniform per wave
+      u32x2 r[2][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = 4 * dg + i;
-        f16x4 h;
+      for (int k = 0; k < 2; ++k) {
+        const int it = it0 + k * stride;
+        if (it < G::TITEMS) {
+          const int kg = it & 15, dg = it >> 4;
+          const int pos = (dg >> 1) ^ (kg & (G::NCH - 1));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t w = r[j][i >> 1];
-          h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+          for (int j = 0; j < 4; ++j) r[k][j] = *(const u32x2*)(rawv + (4 * kg + j) * G::ROWB + pos * 16 + (dg & 1) * 8);
         }
-        *(f16x4*)(vt + d * G::VT_ROWB + ((slot ^ vtswz(d)) * 16) + sub * 8) = h;
+      }
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int it = it0 + k * stride;
+        if (it < G::TITEMS) {
+          const int kg = it & 15, dg = it >> 4;
+          const int slot = ((kg >> 2) << 1) | (kg & 1), sub = (kg >> 1) & 1;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int d = 4 * dg + i;
+            f16x4 h;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t w = r[k][j][i >> 1];
+              h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+            }
+            *(f16x4*)(vt + d * G::VT_ROWB + ((slot ^ vtswz(d)) * 16) + sub * 8) = h;
+          }
+        }
       }
     }
   };
@@ -682,33 +763,61 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    qk(nks, sn);
-    f16x8 pf[2][2];
-    float psum = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
-        psum += p;
-        pf[kt][r >> 3][r & 7] = (_Float16)p;
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
     if (__ballot(alpha != 1.f) != 0) {      // rescale only when some row's running max moved
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) o[dt] *= alpha;
     }
+    m_run = m_new;
+    // From here on one basic block, laid out by hand with scheduling fences: each step issues the
+    // K fragment reads one step ahead, two score MFMAs of the next tile and 32/NQF of this tile's
+    // exponentials (the matrix core works while the vector ALU exponentiates); then the P V MFMAs
+    // with their V fragment reads two ahead.
+    constexpr int EPQ = 32 / NQF;                 // exponentials per score step
+    f16x8 pf[2][2];
+    float psum = 0.f;
+    u32x4 kf[2][2];
+    auto kread = [&](int kq, u32x4 (&dst)[2]) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt) {
+        const int key = kt * 32 + (lane & 31), ch = 2 * kq + half;
+        dst[kt] = *(const u32x4*)(nks + key * G::ROWB + ((ch ^ (key & (G::NCH - 1))) * 16));
+      }
+    };
+    sn[0] = sn[1] = (f32x16){};
+    kread(0, kf[0]);
 #pragma unroll
-      for (int kq = 0; kq < 2; ++kq)
+    for (int kq = 0; kq < NQF; ++kq) {
+      if (kq + 1 < NQF) kread(kq + 1, kf[(kq + 1) & 1]);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          const int d = dt * 32 + (lane & 31);
-          const f16x8 vf = *(const f16x8*)(vt + d * G::VT_ROWB + (((4 * kt + 2 * kq + half) ^ vtswz(d)) * 16));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[kt][kq], o[dt], 0, 0, 0);
-        }
+      for (int kt = 0; kt < 2; ++kt)
+        sn[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kq & 1][kt]),
+                                                         __builtin_bit_cast(bf16x8, qf[kq]), sn[kt], 0, 0, 0);
+#pragma unroll
+      for (int e = kq * EPQ; e < (kq + 1) * EPQ; ++e) {
+        const int kt = e >> 4, r = e & 15;
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
+        psum += p;
+        pf[kt][r >> 3][r & 7] = (_Float16)p;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run = l_run * alpha + psum;
+    constexpr int NPV = 4 * NDT;                  // P V MFMAs per tile
+    f16x8 vf[3];
+    auto vread = [&](int j) __attribute__((always_inline)) -> f16x8 {
+      const int kt = j / (2 * NDT), kq = (j / NDT) & 1, dt = j % NDT;
+      const int d = dt * 32 + (lane & 31);
+      return *(const f16x8*)(vt + d * G::VT_ROWB + (((4 * kt + 2 * kq + half) ^ vtswz(d)) * 16));
+    };
+    vf[0] = vread(0);
+    vf[1] = vread(1);
+#pragma unroll
+    for (int j = 0; j < NPV; ++j) {
+      if (j + 2 < NPV) vf[(j + 2) % 3] = vread(j + 2);
+      const int kt = j / (2 * NDT), kq = (j / NDT) & 1, dt = j % NDT;
+      o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[j % 3], pf[kt][kq], o[dt], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
   // ---- pipeline. step(i): wait for tile i+1, refill the slot tile i used with tile i+3, transpose
@@ -716,19 +825,19 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   f32x16 sa[2], sb[2];
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
     const int sn_ = si == 2 ? 0 : si + 1;
-    lds_barrier_after_dma_wait<D>(i + 2 < n_tiles ? 1 : 0);
-    if (i + 3 < n_tiles) issue(i + 3, ring[si]);
+    attn_sync<D>(npd, dma_wave, i + 2 < n_tiles);
+    if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[si]);
     if (i + 1 < n_tiles) transpose(ring[sn_] + G::TILE, vtr[(i + 1) & 1]);
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
     if (wave_active) finish(i, s, vtr[i & 1], ring[sn_], sn);
   };
   if (n_tiles > 0) {
-    issue(0, ring[0]);
-    if (n_tiles > 1) issue(1, ring[1]);
-    if (n_tiles > 2) issue(2, ring[2]);
-    if (n_tiles > 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * G::LPT) : "memory");
-    else if (n_tiles > 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(G::LPT) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (dma_wave) {
+      issue(0, ring[0]);
+      if (n_tiles > 1) issue(1, ring[1]);
+    }
+    attn_sync<D>(npd, dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
+    if (dma_wave && n_tiles > 2) issue(2, ring[2]);
     transpose(ring[0] + G::TILE, vtr[0]);
     if (wave_active) qk(ring[0], sa);
     int si = 0;
