@@ -25,7 +25,9 @@
  *   call returns without synchronising; faults inside kernels surface at the
  *   caller's next synchronisation.
  * - `workspace` is device scratch of at least the size the matching
- *   *_workspace query returns (which may be 0, and then `workspace` may be NULL).
+ *   *_workspace query returns (which may be 0, and then `workspace` may be NULL);
+ *   it must be 256-byte aligned. Bulk operand and output arrays (hidden, A, bias,
+ *   W, logits, z, q, caches, target_logits) must be 16-byte aligned.
  * - Arguments are checked on the host before anything is enqueued. A failed
  *   check returns a non-zero sr_status, leaves every output untouched and sets a
  *   thread-local message readable through sr_last_error().
@@ -110,8 +112,8 @@ size_t sr_heads_propose_workspace(const sr_heads_desc* desc);
  * parents     [B,T]    int32   tree topology (see conventions)
  * root_token  [B]      int32   the anchor token, already sampled
  * u_tree      [B,T]    fp32    uniforms in (0,1); entry c orders the slot node c fills
- * logits      [B,H,V]  fp32    OUT (optional, NULL = keep in workspace)
- * z           [B,H,d]  dtype   OUT (optional, NULL = keep in workspace)
+ * logits      [B,H,V]  fp32    OUT (optional, NULL = keep in workspace); 16-byte aligned
+ * z           [B,H,d]  dtype   OUT (optional, NULL = keep in workspace); 16-byte aligned
  * tokens      [B,T]    int32   OUT; tokens[b][0] = root_token[b]
  * child_logit [B,T]    fp32    OUT; head logit of tokens[b][c] under the proposing
  *                              head; 0 at the root

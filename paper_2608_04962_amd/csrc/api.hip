@@ -164,6 +164,7 @@ sr_status sr_heads_propose(const sr_heads_desc* d, const void* hidden, const flo
            "a required pointer is null");
   SR_CHECK(aligned16(hidden) && aligned16(A) && aligned16(W) && aligned16(bias), "hidden/A/bias/W must be 16-byte aligned");
   SR_CHECK(z == nullptr || aligned16(z), "z must be 16-byte aligned");
+  SR_CHECK(logits == nullptr || aligned16(logits), "logits must be 16-byte aligned");
   const HeadsLayout L = heads_layout(*d, z == nullptr, logits == nullptr);
   st = check_ws(workspace, workspace_bytes, L.total);
   if (st != SR_OK) return st;

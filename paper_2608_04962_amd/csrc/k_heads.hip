@@ -84,7 +84,9 @@ template <typename T>
 struct EpiHead {
   const T* bias; const float* x; T* z; int d, H;
   static constexpr bool kGroupMax = false;
+  static constexpr bool kTrans = false;
   __device__ __forceinline__ void group_max(int, int, float) const {}
+  __device__ __forceinline__ void store4(int, int, f32x4) const {}
   __device__ __forceinline__ void operator()(int m, int n, float acc) const {
     const int h = n / d, j = n - h * d;
     const float v = acc + Elem<T>::load(bias, n);
@@ -193,19 +195,24 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
 
 // ============================================================================ bf16 GEMM, direct-to-LDS
 // C[m][n] = sum_k A[m][k] * B[n][k] for bf16 operands (both K-contiguous). Tiles stream from global
-// memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring, so STAGES-1 K-steps are
-// in flight while one is multiplied. In LDS a tile row of BK elements is CPR 16-byte chunks; chunk c of
-// row r is stored at position c ^ ((r >> 1) & (CPR - 1)), which keeps the 32x32x16 MFMA operand reads
-// free of bank conflicts. Blocks are mapped so that the M-tiles sharing one N-tile of B run on the same
-// XCD at the same time (B is read from HBM once and hits in that XCD's L2 for the others).
+// memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring: while K-step ks is
+// multiplied, steps up to ks+STAGES-2 are in flight, and the MFMA operand fragments of step ks+1 are read
+// into registers between the two halves of step ks's MFMAs (one barrier per K-step). In LDS a tile row of
+// BK elements is CPR 16-byte chunks; chunk c of row r is stored at position c ^ ((r >> 1) & (CPR - 1)),
+// which keeps the 32x32x16 MFMA operand reads free of bank conflicts. Blocks are mapped so that the
+// M-tiles sharing one N-tile of B run on the same XCD at the same time (B is read from HBM once and hits
+// in that XCD's L2 for the others).
 // Epilogue of the vocabulary GEMM: fp32 logits[m][n] plus, per row, the max over each 64-column group
-// (the top-M selection scans only groups whose max can reach the M-th largest value).
+// (the top-M selection scans only groups whose max can reach the M-th largest value). It takes the
+// transposed accumulator layout (a lane owns one row and runs of four consecutive columns), so the
+// logits leave as 16-byte stores and a group max needs one cross-lane exchange. Requires N % 4 == 0.
 struct EpiLogitsMax {
   float* out; float* gmax; int N, ngroups;
   static constexpr bool kGroupMax = true;
-  __device__ __forceinline__ void operator()(int m, int n, float acc) const { out[(size_t)m * N + n] = acc; }
+  static constexpr bool kTrans = true;
+  __device__ __forceinline__ void store4(int m, int n, f32x4 v) const { *(f32x4*)(out + (size_t)m * N + n) = v; }
   __device__ __forceinline__ void group_max(int m, int grp, float v) const {
-    if (grp < ngroups) gmax[(size_t)m * ngroups + grp] = v;   // a tile's last wave may lie past V
+    if (grp < ngroups) gmax[(size_t)m * ngroups + grp] = v;   // a tile's last wave may lie past N
   }
 };
 
@@ -224,12 +231,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert((A_BLK + B_BLK) % NW == 0 && A_BLK % NW == 0, "DMA blocks must split evenly over the waves");
   static_assert(CPR >= 2 && (CPR & (CPR - 1)) == 0 && BK % 16 == 0, "tile");
-  static_assert(STAGES == 4, "the K loop below is unrolled over four LDS stages");
-  // one LDS array per stage, so the compiler can tell the stages' DMA writes apart
-  __shared__ __attribute__((aligned(1024))) unsigned char lds0[A_BYTES + B_BYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char lds1[A_BYTES + B_BYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char lds2[A_BYTES + B_BYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char lds3[A_BYTES + B_BYTES];
+  static_assert(STAGES == 4 || STAGES == 5, "ring of four or five stages");
+  static_assert(3 * LPS <= 63, "three stages of DMA per wave must fit the vmcnt counter");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES][A_BYTES + B_BYTES];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -257,12 +261,22 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
     const int c = pos ^ ((r >> 1) & (CPR - 1));
     srcB[j] = (const unsigned char*)(B + (size_t)min(n0 + r, N - 1) * K) + c * 16;
   }
-  auto issue = [&](int ks, unsigned char* dst) {
+  // the transfers are untracked by the compiler: every wait on them below is explicit
+  auto issue = [&](int ks) {
+    unsigned char* dst = lds[ks % STAGES];
     const size_t koff = (size_t)ks * ROWB;
 #pragma unroll
-    for (int j = 0; j < A_BLK / NW; ++j) lds_dma16(srcA[j] + koff, dst + (wave + j * NW) * 1024);
+    for (int j = 0; j < A_BLK / NW; ++j) lds_dma16_manual(srcA[j] + koff, dst + (wave + j * NW) * 1024);
 #pragma unroll
-    for (int j = 0; j < B_BLK / NW; ++j) lds_dma16(srcB[j] + koff, dst + A_BYTES + (wave + j * NW) * 1024);
+    for (int j = 0; j < B_BLK / NW; ++j) lds_dma16_manual(srcB[j] + koff, dst + A_BYTES + (wave + j * NW) * 1024);
+  };
+  // stage ks has landed for the whole block (the STAGES-3 stages after it may still be in flight) and every
+  // wave's LDS reads are done
+  auto sync = [&](int ks) {
+    const int ahead = min(STAGES - 3, nk - 1 - ks);
+    if (ahead >= 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPS) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPS) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
 
   f32x16 acc[TM][TN];
@@ -271,105 +285,104 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
 
-  // fragment addresses: lane reads row (l%32) of a 32-row group at chunk 2*kk + l/32 (swizzled)
+  // fragments: lane reads row (l%32) of a 32-row group at chunk 2*kk + l/32 (swizzled)
   const int fr = lane & 31, fh = lane >> 5;
-  auto mma_step = [&](const unsigned char* As) {
+  struct Frags { u32x4 a[BK / 16][TM], b[BK / 16][TN]; };
+  auto load = [&](int ks, Frags& f) {
+    const unsigned char* As = lds[ks % STAGES];
     const unsigned char* Bs = As + A_BYTES;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       const int c = 2 * kk + fh;
-      u32x4 fa[TM], fb[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = wm * WTM + i * 32 + fr;
-        fa[i] = *(const u32x4*)(As + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
+        f.a[kk][i] = *(const u32x4*)(As + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = wn * WTN + j * 32 + fr;
-        fb[j] = *(const u32x4*)(Bs + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[i]),
-                                                              __builtin_bit_cast(bf16x8, fb[j]), acc[i][j], 0, 0, 0);
-    }
-  };
-  // one K-step: wait for this stage's DMA (the next two steps' may stay in flight), make it visible to
-  // the block, refill the stage consumed one step ago, multiply
-  auto step = [&](int ks, unsigned char* cur, unsigned char* refill) {
-    const int ahead = min(2, nk - 1 - ks);
-    if (ahead >= 2) wait_vmcnt<2 * LPS>();
-    else if (ahead == 1) wait_vmcnt<LPS>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (ks + 3 < nk) issue(ks + 3, refill);
-    mma_step(cur);
-  };
-  if (0 < nk) issue(0, lds0);
-  if (1 < nk) issue(1, lds1);
-  if (2 < nk) issue(2, lds2);
-  for (int ks = 0; ks < nk; ks += 4) {
-    step(ks, lds0, lds3);
-    if (ks + 1 < nk) step(ks + 1, lds1, lds0);
-    if (ks + 2 < nk) step(ks + 2, lds2, lds1);
-    if (ks + 3 < nk) step(ks + 3, lds3, lds2);
-  }
-
-  // epilogue: element stores (lane column l%32, register r -> row 8*(r/4) + 4*(l/32) + r%4)
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn * WTN + j * 32 + fr;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
-        if (m < M && n < N) epi(m, n, acc[i][j][r]);
+        f.b[kk][j] = *(const u32x4*)(Bs + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
       }
     }
-  if constexpr (Epi::kGroupMax) {
-    static_assert(WTN == 64 && TM * 16 == 64, "group max assumes 64 columns and 64 row slots per lane");
-    // row max over the wave's 64 columns: fold the two 32-column tiles, then reduce across the 32 lanes of
-    // each half by recursive halving (after 5 exchanges a lane owns the maxima of 2 of its 64 row slots)
-    float v[64];
+  };
+  auto mma = [&](const Frags& f, int kk) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float a = -INFINITY;
+      for (int j = 0; j < TN; ++j)
+        if constexpr (Epi::kTrans)   // C^T tile: lane <-> row m, registers <-> columns n
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.b[kk][j]),
+                                                              __builtin_bit_cast(bf16x8, f.a[kk][i]), acc[i][j], 0, 0, 0);
+        else                         // C tile: lane <-> column n, registers <-> rows m
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.a[kk][i]),
+                                                              __builtin_bit_cast(bf16x8, f.b[kk][j]), acc[i][j], 0, 0, 0);
+  };
+  // K-step ks: half of its MFMAs; wait for stage ks+1 and meet the block (every wave is done reading stage
+  // ks-1); refill stage ks-1 with step ks+STAGES-1; read step ks+1's fragments; the other half
+  static_assert(BK / 16 == 2, "two MFMA halves per K-step");
+  auto step = [&](int ks, const Frags& cur, Frags& nxt) {
+    mma(cur, 0);
+    if (ks + 1 < nk) {
+      sync(ks + 1);
+      if (ks + STAGES - 1 < nk) issue(ks + STAGES - 1);
+      load(ks + 1, nxt);
+    }
+    mma(cur, 1);
+  };
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int n = n0 + wn * WTN + j * 32 + fr;
-          a = fmaxf(a, n < N ? acc[i][j][r] : -INFINITY);
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < nk) issue(t);
+  {
+    const int ahead = min(STAGES - 2, nk - 1);   // stages issued after stage 0
+    if (ahead >= 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(3 * LPS) : "memory");
+    else if (ahead == 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPS) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPS) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+  Frags fa_, fb_;
+  load(0, fa_);
+  for (int ks = 0; ks < nk; ks += 2) {
+    step(ks, fa_, fb_);
+    if (ks + 1 < nk) step(ks + 1, fb_, fa_);
+  }
+
+  if constexpr (Epi::kTrans) {
+    // lane owns row m = .. + l%32; register r of tile j holds column 32*j + 8*(r/4) + 4*(l/32) + r%4
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + wm * WTM + i * 32 + fr;
+      float gm = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * fh;
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          if (n < N) {
+            if (m < M) epi.store4(m, n, v);
+            gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+          }
         }
-        v[i * 16 + r] = a;
-      }
-#pragma unroll
-    for (int step = 0; step < 5; ++step) {
-      const int half_n = 32 >> step;           // values kept after this step
-      const int off = 16 >> step;              // lane distance of the exchange
-      const bool upper = (fr & off) != 0;
-#pragma unroll
-      for (int q = 0; q < half_n; ++q) {
-        const float keep = upper ? v[q + half_n] : v[q];
-        const float send = upper ? v[q] : v[q + half_n];
-        const float recv = __shfl_xor(send, off, 64);
-        v[q] = fmaxf(keep, recv);
+      if constexpr (Epi::kGroupMax) {
+        static_assert(WTN == 64, "one 64-column group per wave");
+        gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
+        if (fh == 0 && m < M) epi.group_max(m, (n0 + wn * WTN) / 64, gm);
       }
     }
-    // this lane owns slots s0 and s0 + 1, s0 = sum over exchanged bits
-    const int s0 = ((fr >> 4) & 1) * 32 + ((fr >> 3) & 1) * 16 + ((fr >> 2) & 1) * 8 + ((fr >> 1) & 1) * 4 +
-                   (fr & 1) * 2;
-    const int grp = (n0 + wn * WTN) / 64;
+  } else {
+    // element stores (lane column l%32, register r -> row 8*(r/4) + 4*(l/32) + r%4)
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int slot = s0 + e, i = slot >> 4, r = slot & 15;
-      const int m = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
-      if (m < M) epi.group_max(m, grp, v[e]);
-    }
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + wn * WTN + j * 32 + fr;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
+          if (m < M && n < N) epi(m, n, acc[i][j][r]);
+        }
+      }
   }
 }
 
@@ -674,7 +687,7 @@ static sr_status launch_heads_t(const sr_heads_desc& d, const void* hidden, cons
       EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
       const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
       dim3 grid(((tn + 7) / 8) * 8 * tm);
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 4, EpiLogitsMax>), grid, dim3(512), 0, s,
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), grid, dim3(512), 0, s,
                 (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
     }
   } else {
