@@ -8,7 +8,7 @@
 //
 // One block (16 waves) walks one trajectory. At each visited node the block makes a single
 // pass over the target-logit row: every wave reduces 512-token chunks to (chunk max, sum of
-// exp(logit - chunk max)) with fp32 exponentials summed in float64. The residual is only
+// exp(logit - chunk max)) in fp32; the chunk sums are combined in float64. The residual is only
 // ever different from p on the node's children, so wave 0 keeps it explicitly on the
 // children (float64) plus one scalar for the mass outside them; the slot tests and the
 // normaliser Z are exact restatements of the full-vocabulary update. Terminal draws walk the
@@ -61,10 +61,10 @@ struct AccSmem {
   double draw_margin;
 };
 
-// exp(y - m) with y = x * invtau and the subtraction rounded separately, so the value is
-// identical wherever it is recomputed
+// exp(y - m) with y = x * invtau, as 2^((y - m) log2 e) on the hardware exponential; every step is
+// rounded separately, so the value is identical wherever it is recomputed
 __device__ __forceinline__ float tilt(float x, float invtau, float m) {
-  return expf(__fsub_rn(__fmul_rn(x, invtau), m));
+  return __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(__fmul_rn(x, invtau), m), kLog2e));
 }
 
 template <typename T>
@@ -89,27 +89,27 @@ __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float i
       float ml = -INFINITY;
 #pragma unroll
       for (int e = 0; e < 8; ++e) ml = fmaxf(ml, __fmul_rn(x[gi][e], invtau));
-      const float m = warp_max(ml);
-      double sl = 0.0;
+      const float m = wave_max_f32(ml);
+      float sl = 0.f;                           // at most 512 terms in (0, 1]: fp32 suffices
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (x[gi][e] != -INFINITY) sl += (double)tilt(x[gi][e], invtau, m);
-      const double s = warp_sum_d(sl);
-      if (lane == 0) { sm.cmax[c0 + gi] = m; sm.csum[c0 + gi] = s; }
+        if (x[gi][e] != -INFINITY) sl += tilt(x[gi][e], invtau, m);
+      const float s = wave_sum_f32(sl);
+      if (lane == 0) { sm.cmax[c0 + gi] = m; sm.csum[c0 + gi] = (double)s; }
     }
   }
   __syncthreads();
   if (wave == 0) {
     float ml = -INFINITY;
     for (int c = lane; c < nch; c += 64) ml = fmaxf(ml, sm.cmax[c]);
-    const float M = warp_max(ml);
+    const float M = wave_max_f32(ml);
     double sl = 0.0;
     for (int c = lane; c < nch; c += 64) {
       const double sc = exp((double)sm.cmax[c] - (double)M);
       sm.cscale[c] = sc;
       sl += sm.csum[c] * sc;
     }
-    const double S = warp_sum_d(sl);
+    const double S = wave_sum_f64(sl);
     if (lane == 0) sm.S = S;
   }
   __syncthreads();
@@ -329,7 +329,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
           out_mass_part += pt;
         }
       }
-      double rest = (sm.S - warp_sum_d(out_mass_part)) / sm.S;
+      double rest = (sm.S - wave_sum_f64(out_mass_part)) / sm.S;
       int acc = -1;
       for (int j = 0; j < m; ++j) {
         // q_{u,j}: softmax of the draft logits over children j..m-1
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
 #pragma unroll
         for (int s = 0; s < 2; ++s)
           if (lane + 64 * s >= j) mx = fmax(mx, lg[s]);
-        mx = warp_max_d(mx);
+        mx = wave_max_f64(mx);
         double w[2];
         double ql = 0.0;
 #pragma unroll
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
           w[s] = (k >= j && k < m) ? exp(lg[s] - mx) : 0.0;
           ql += w[s];
         }
-        const double Q = warp_sum_d(ql);
+        const double Q = wave_sum_f64(ql);
         const double rj = __shfl((j >> 6) ? r[1] : r[0], j & 63, 64);
         const double qj = __shfl((j >> 6) ? w[1] : w[0], j & 63, 64) / Q;
         const double A = fmin(1.0, rj / qj);
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
           if (k >= j && k < m) r[s] = fmax(r[s] - w[s] / Q, 0.0);
           zl += (k < m) ? r[s] : 0.0;
         }
-        const double Z = rest + warp_sum_d(zl);
+        const double Z = rest + wave_sum_f64(zl);
         rest /= Z;
 #pragma unroll
         for (int s = 0; s < 2; ++s) r[s] /= Z;
