@@ -602,66 +602,94 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restric
 }
 
 // ============================================================================ tree build
-// One block per trajectory, one thread per node: node u draws the ordered list of its m_u
-// children from C_u = top-m_u of head min(depth(u)+1, H), without replacement (Eq. (slotq)).
-__global__ __launch_bounds__(SR_MAX_TREE) void k_tree_build(const int32_t* __restrict__ top_id,
-                                                            const float* __restrict__ top_val, int H, int M, int T,
-                                                            const int32_t* __restrict__ parents,
-                                                            const int32_t* __restrict__ root_token,
-                                                            const float* __restrict__ u_tree,
-                                                            int32_t* __restrict__ tokens,
-                                                            float* __restrict__ child_logit) {
+// One block per trajectory, one wave per node with children: node u draws the ordered list of its
+// m_u children from C_u = top-m_u of head min(depth(u)+1, H), without replacement (Eq. (slotq)).
+// The wave holds C_u across its lanes, so each draw's float64 weights, their sum and the cumulative
+// weights in C_u's order are computed in parallel.
+constexpr int TB_NT = 256;
+__global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict__ top_id,
+                                                     const float* __restrict__ top_val, int H, int M, int T,
+                                                     const int32_t* __restrict__ parents,
+                                                     const int32_t* __restrict__ root_token,
+                                                     const float* __restrict__ u_tree,
+                                                     int32_t* __restrict__ tokens,
+                                                     float* __restrict__ child_logit) {
   __shared__ TreeLds<SR_MAX_TREE> t;
   __shared__ int too_many;
-  const int b = blockIdx.x, u = threadIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   bool ok = tree_setup<SR_MAX_TREE>(t, parents + (size_t)b * T, T);
   if (ok) {
-    if (u == 0) too_many = 0;
+    if (tid == 0) too_many = 0;
     __syncthreads();
-    if (u < T && t.nkids[u] > M) atomicOr(&too_many, 1);
+    if (tid < T && t.nkids[tid] > M) atomicOr(&too_many, 1);
     __syncthreads();
     ok = !too_many;
   }
   int32_t* tok_b = tokens + (size_t)b * T;
   float* cl_b = child_logit + (size_t)b * T;
   if (!ok) {
-    if (u < T) {
+    for (int u = tid; u < T; u += TB_NT) {
       tok_b[u] = u == 0 ? root_token[b] : -1;
       cl_b[u] = u == 0 ? 0.f : __uint_as_float(0x7fc00000u);
     }
     return;
   }
-  if (u == 0) { tok_b[0] = root_token[b]; cl_b[0] = 0.f; }
-  if (u >= T) return;
-  const int m = t.nkids[u];
-  if (m == 0) return;
-  const int k = min(t.depth[u] + 1, H);                       // proposing head, 1-based
-  const size_t rbase = ((size_t)b * H + (k - 1)) * M;
-  uint32_t used[SR_MAX_TREE / 32] = {0, 0, 0, 0};
-  int c = u + 1;
-  for (int j = 0; j < m; ++j) {
-    while (t.parent[c] != u) ++c;                              // j-th child of u in index order
-    // weights exp(l - max over the remaining candidates), float64, in C_u's order
-    double mx = -INFINITY;
-    for (int i = 0; i < m; ++i)
-      if (!((used[i >> 5] >> (i & 31)) & 1u)) mx = fmax(mx, (double)top_val[rbase + i]);
-    double S = 0.0;
-    for (int i = 0; i < m; ++i)
-      if (!((used[i >> 5] >> (i & 31)) & 1u)) S += exp((double)top_val[rbase + i] - mx);
-    const double target = (double)u_tree[(size_t)b * T + c] * S;
-    double cum = 0.0;
-    int pick = -1, last = -1;
-    for (int i = 0; i < m; ++i) {
-      if ((used[i >> 5] >> (i & 31)) & 1u) continue;
-      cum += exp((double)top_val[rbase + i] - mx);
-      last = i;
-      if (target < cum) { pick = i; break; }
+  if (tid == 0) { tok_b[0] = root_token[b]; cl_b[0] = 0.f; }
+  // one wave per node with children; lane i holds candidates i and i + 64 of C_u
+  for (int u = wave; u < T; u += TB_NT / 64) {
+    const int m = t.nkids[u];
+    if (m == 0) continue;                                      // uniform per wave
+    const int k = min(t.depth[u] + 1, H);                      // proposing head, 1-based
+    const size_t rbase = ((size_t)b * H + (k - 1)) * M;
+    double l[2];
+    bool live[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int i = lane + 64 * s2;
+      live[s2] = i < m;
+      l[s2] = live[s2] ? (double)top_val[rbase + i] : -INFINITY;
     }
-    if (pick < 0) pick = last;                                 // rounding guard: U*S at the very top
-    used[pick >> 5] |= 1u << (pick & 31);
-    tok_b[c] = top_id[rbase + pick];
-    cl_b[c] = top_val[rbase + pick];
-    ++c;
+    int c = u + 1;
+    for (int j = 0; j < m; ++j) {
+      while (t.parent[c] != u) ++c;                            // j-th child of u in index order
+      // weights exp(l - max over the remaining candidates), float64, in C_u's order
+      const double mx = wave_max_f64(fmax(live[0] ? l[0] : -INFINITY, live[1] ? l[1] : -INFINITY));
+      double w[2];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) w[s2] = live[s2] ? exp(l[s2] - mx) : 0.0;
+      // inclusive prefix sums over candidates 0..63, then 64..127
+      double cum[2];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        double v = w[s2];
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const double y = __shfl_up(v, o, 64);
+          if (lane >= o) v += y;
+        }
+        cum[s2] = v;
+      }
+      const double tot0 = __shfl(cum[0], 63, 64);
+      cum[1] += tot0;
+      const double S = __shfl(cum[1], 63, 64);
+      const double target = (double)u_tree[(size_t)b * T + c] * S;
+      // first candidate whose cumulative weight exceeds the target; the last live one on rounding
+      const unsigned long long hit0 = __ballot(live[0] && target < cum[0]);
+      const unsigned long long hit1 = __ballot(live[1] && target < cum[1]);
+      int pick;
+      if (hit0) pick = __ffsll((long long)hit0) - 1;
+      else if (hit1) pick = 64 + __ffsll((long long)hit1) - 1;
+      else {
+        const unsigned long long l1 = __ballot(live[1]), l0 = __ballot(live[0]);
+        pick = l1 ? 64 + 63 - __clzll((long long)l1) : 63 - __clzll((long long)l0);
+      }
+      if (lane == (pick & 63)) live[pick >> 6] = false;
+      if (lane == 0) {
+        tok_b[c] = top_id[rbase + pick];
+        cl_b[c] = top_val[rbase + pick];
+      }
+      ++c;
+    }
   }
 }
 
@@ -737,7 +765,7 @@ sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const f
                 (const int*)nullptr);
     }
   }
-  SR_LAUNCH("sr_tree_build", k_tree_build, dim3(d.B), dim3(SR_MAX_TREE), 0, s, top_id, top_val, d.H, M, d.T,
+  SR_LAUNCH("sr_tree_build", k_tree_build, dim3(d.B), dim3(TB_NT), 0, s, top_id, top_val, d.H, M, d.T,
             parents, root_token, u_tree, tokens, child_logit);
   return SR_OK;
 }
