@@ -12,6 +12,9 @@ from the paper (SpecRoll, arXiv 2608.04962):
 * ``accept``    -- exact node-wise verification with full-vocabulary
                    residuals (App. B.2, Eq. (nodeaccept), Eq. (noderesidual),
                    Alg. "Exact node-wise tree verification").
+* ``engine``    -- the concurrency-aware node budget and the tree it allows
+                   (Sec. 3.3, Eq. (verification-budget), Eq. (tree-budget)) and
+                   the accepted-path cache extraction.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may use this package. It shares no code with the HIP library and
@@ -22,3 +25,4 @@ from .heads import clip_correction, layer_norm, silu, heads_forward  # noqa: F40
 from .tree import tree_structure, top_m, sample_ordered_children, tree_build  # noqa: F401
 from .attention import gather_prefix, tree_attention, tree_attention_node  # noqa: F401
 from .accept import inverse_cdf, tree_accept, tree_accept_one, FALLBACK, BONUS  # noqa: F401
+from .engine import tree_budget, commit_path  # noqa: F401

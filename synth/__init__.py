@@ -27,6 +27,7 @@ _TID = {
     "q": 20, "kc": 21, "vc": 22, "kt": 23, "vt": 24, "ctx": 25, "perm": 26,
     "tlogits": 40, "dnoise": 41, "order": 42, "u_acc": 43, "u_fin": 44,
     "hlogits": 50,
+    "ckc": 60, "cvc": 61, "ckt": 62, "cvt": 63, "cacc": 64, "cperm": 65,
 }
 
 
@@ -360,4 +361,64 @@ def accept_inputs(cfg: Config, seed: int = 0, target_std: float = 4.0, noise_std
         u_acc=uniforms(_rng(seed, cfg, "u_acc"), (B, T)),
         u_fin=uniforms(_rng(seed, cfg, "u_fin"), (B,)),
         max_depth=int(node_depths(par).max()) if T > 1 else 0,
+    )
+
+
+def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1) -> dict:
+    """Inputs of the accepted-path cache extraction, stacked over ``n_layers`` layers.
+
+    Each trajectory's page list has room for its prefix plus a full root path (depth + 1 rows).
+    The accepted path is a random root path of a random target length 0..depth (at every step a
+    uniformly chosen child among those whose subtree reaches that length, else among all children,
+    stopping early at a leaf); out_len = 1 + its length. Cache slots past the prefix hold
+    NaN, so a row that is not written stays visibly untouched.
+    """
+    B, T, Hkv, D, bs = cfg.B, cfg.T, cfg.Hkv, cfg.D, cfg.block_size
+    par = topology(cfg)
+    dep = node_depths(par)
+    max_depth = int(dep.max()) if T > 1 else 0
+    L = context_lengths(cfg, seed)
+    nblk = -(-(L + max_depth + 1) // bs)
+    num_blocks = int(nblk.sum())
+    max_blocks = int(nblk.max())
+    phys = (np.arange(num_blocks, dtype=np.int32) if cfg.contiguous_pages
+            else _rng(seed, cfg, "cperm").permutation(num_blocks).astype(np.int32))
+    table = np.full((B, max_blocks), -1, dtype=np.int32)
+    off = 0
+    for b in range(B):
+        table[b, :nblk[b]] = phys[off:off + nblk[b]]
+        off += nblk[b]
+    kc = normal(_rng(seed, cfg, "ckc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
+    vc = normal(_rng(seed, cfg, "cvc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
+    for b in range(B):
+        pos = np.arange(int(L[b]), int(nblk[b]) * bs)
+        kc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
+        vc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
+    kids = [[] for _ in range(T)]
+    for c in range(1, T):
+        kids[par[c]].append(c)
+    reach = dep.copy()                 # deepest depth inside each node's subtree
+    for c in range(T - 1, 0, -1):
+        reach[par[c]] = max(reach[par[c]], reach[c])
+    rng = _rng(seed, cfg, "cacc")
+    acc = np.full((B, max(1, max_depth)), -1, dtype=np.int32)
+    out_len = np.empty(B, dtype=np.int32)
+    for b in range(B):
+        want = int(rng.integers(0, max_depth + 1))
+        u, n = 0, 0
+        while n < want and kids[u]:
+            deep = [c for c in kids[u] if reach[c] >= want]
+            pick = deep if deep else kids[u]
+            u = pick[int(rng.integers(0, len(pick)))]
+            acc[b, n] = u
+            n += 1
+        out_len[b] = n + 1
+    return dict(
+        cfg=cfg, dtype=cfg.dtype, n_layers=n_layers, ctx_len=L.astype(np.int32), block_table=table,
+        num_blocks=num_blocks, max_blocks=max_blocks, max_depth=max(1, max_depth),
+        k_cache=as_dtype(kc, cfg.dtype), v_cache=as_dtype(vc, cfg.dtype),
+        k_tree=as_dtype(normal(_rng(seed, cfg, "ckt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
+        v_tree=as_dtype(normal(_rng(seed, cfg, "cvt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
+        parents=np.ascontiguousarray(np.broadcast_to(par, (B, T))).astype(np.int32),
+        acc_nodes=acc, out_len=out_len,
     )
