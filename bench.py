@@ -4,6 +4,8 @@ A step is the whole hot path over one batch of synthetic inputs resident in HBM:
   sr_heads_propose (heads + vocabulary projection + draft tree)
   -> sr_tree_verify_attn (tree-masked attention over the paged prefix, one layer)
   -> sr_tree_accept (exact acceptance walk).
+After the timed steps, the accepted-path cache commit (sr_commit_path) of the last step's accepted
+paths is timed on its own for all 28 layers of the 7B-shaped target and reported beside the step.
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
 hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
 
@@ -29,7 +31,8 @@ CALIB_ELEMS = 1 << 28          # 1 GiB of float32 read and 1 GiB written by the 
 KERNEL_SOURCE = {"sr_tree_attn": "k_attn.hip", "sr_attn_combine": "k_attn.hip", "sr_vocab_gemm": "k_heads.hip",
                  "sr_head_gemm": "k_heads.hip", "sr_clip_ln": "k_heads.hip", "sr_group_max": "k_heads.hip",
                  "sr_topm": "k_heads.hip", "sr_topm_full": "k_heads.hip", "sr_tree_build": "k_heads.hip",
-                 "sr_tree_accept": "k_accept.hip"}
+                 "sr_tree_accept": "k_accept.hip", "sr_commit_path": "k_engine.hip"}
+COMMIT_LAYERS = 28             # decoder layers of the 7B-shaped target: one commit launch covers all of them
 
 
 def log(msg):
@@ -192,9 +195,47 @@ def main():
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
     }
 
+    res["commit_path"] = commit_bench(sr, synth, cfg, args.seed, outs, dev)
+    res["tree_budget"] = dict(zip(("N_t", "horizon_counts", "parents"), sr.tree_budget(B)))
+
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, hin, ain, cin, args.cpu_sample)
     print(json.dumps(res), flush=True)
+
+
+def commit_bench(sr, synth, cfg, seed, outs, dev):
+    """Time sr_commit_path on the step's own accepted paths for every layer of the target (one launch)."""
+    import torch
+    ci = synth.commit_inputs(cfg, seed=seed, with_kv=False)
+    nl, B, T, Hkv, D = COMMIT_LAYERS, cfg.B, cfg.T, cfg.Hkv, cfg.D
+    g = torch.Generator(device=dev).manual_seed(seed)
+    kt = torch.randn((nl, B, T, Hkv, D), generator=g, device=dev).to(torch.bfloat16)
+    vt = torch.randn((nl, B, T, Hkv, D), generator=g, device=dev).to(torch.bfloat16)
+    shape = (nl, ci["num_blocks"], Hkv, cfg.block_size, D)
+    kc = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    vc = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    table = torch.from_numpy(ci["block_table"]).to(dev)
+    ctx = torch.from_numpy(ci["ctx_len"]).to(dev)
+    new = torch.empty((B,), dtype=torch.int32, device=dev)
+    par = torch.from_numpy(ci["parents"]).to(dev)
+    run = lambda: sr.commit_path(kc, vc, table, ctx, kt, vt, outs["acc_nodes"], outs["out_len"],  # noqa: E731
+                                 parents=par, new_ctx_len=new)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    sr.prof_begin("sr_commit_path")
+    for _ in range(20):
+        run()
+    ms, n = sr.prof_end()
+    rows = int(outs["out_len"].sum().item())
+    assert (new.cpu() >= 0).all(), "rejected trajectories in the commit benchmark"
+    moved = rows * Hkv * D * 2 * 2 * nl            # K and V rows, bf16, per layer
+    alg = 2 * moved + B * (4 * 3 + 4 * outs["acc_nodes"].shape[1])  # read + write, plus the small int inputs
+    avg = ms / max(n, 1)
+    del kc, vc, kt, vt
+    torch.cuda.empty_cache()
+    return {"layers": nl, "rows_per_layer": rows, "avg_ms": avg, "launches": n, "algorithmic_bytes": alg,
+            "GB/s": alg / (avg / 1e3) / 1e9, "frac_hbm_peak": alg / (avg / 1e3) / 1e9 / HBM_PEAK_GBPS}
 
 
 def measured_traffic(kernel):

@@ -14,6 +14,11 @@
  *   3. sr_tree_accept       exact node-wise speculative acceptance walk
  *                           (App. B.2 Eq. (nodeaccept), Eq. (noderesidual),
  *                           Alg. "Exact node-wise tree verification").
+ *   4. sr_commit_path       the accepted path's K/V rows appended to the paged
+ *                           cache, every layer in one launch.
+ *      sr_tree_budget       host rule for the per-response node budget and the
+ *                           tree it allows (Sec. 3.2 Eq. (verification-budget),
+ *                           Eq. (tree-budget)).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -231,6 +236,94 @@ sr_status sr_tree_accept(const sr_accept_desc* desc,
                          int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len,
                          uint8_t* final_kind, float* min_margin,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ========================================================================== *
+ * 4. Engine glue around the step
+ * ========================================================================== *
+ * Concurrency-aware node budget (Sec. 3.2 Eq. (verification-budget) and
+ * Eq. (tree-budget); App. C "Implementation and Reproducibility Details",
+ * paragraph "Concurrency-aware sparse tree verification"). With `live`
+ * unfinished responses, each response gets
+ *   N_t = clip(floor(c_peak / live), n_min, n_max)
+ * tree nodes, the anchor counted once. Horizon h = 1, 2, ... receives
+ * min(alloc[h-1], nodes still left of N_t - 1), shallowest first; the first
+ * horizon that receives none ends the tree. Node k (0-based) of horizon h hangs
+ * under node floor(k * n_{h-1} / n_h) of horizon h-1, and nodes are numbered
+ * breadth-first, so `parents` is a valid topology for the calls above. The
+ * paper's settings are c_peak 512, n_min 1, n_max 10 and alloc {5, 4, 0}.
+ * Host-only: every pointer of this call is a HOST pointer and nothing touches
+ * a GPU.
+ */
+typedef struct {
+  int32_t c_peak;        /* profiled verification capacity, nodes per step, >= 1    */
+  int32_t n_min, n_max;  /* 1 <= n_min <= n_max <= SR_MAX_TREE                       */
+  int32_t n_alloc;       /* horizons listed in alloc, 0..SR_MAX_TREE                  */
+  const int32_t* alloc;  /* HOST [n_alloc] nominal non-root nodes per horizon, >= 0   */
+} sr_budget_desc;
+
+/*
+ * live          unfinished responses B_t, >= 1
+ * n_t           OUT    the budget N_t
+ * horizon_count OUT    HOST [n_alloc] (NULL = not written) nodes given to each
+ *                      horizon, 0 from the first empty horizon on
+ * parents       OUT    HOST [parents_cap] the tree's topology; entries past
+ *                      n_nodes are not written
+ * n_nodes       OUT    tree size 1 + sum(horizon_count), <= n_t
+ * parents_cap >= n_max always suffices; a smaller capacity that cannot hold the
+ * tree is an SR_ERR_INVALID with nothing written.
+ */
+sr_status sr_tree_budget(const sr_budget_desc* desc, int32_t live, int32_t* n_t, int32_t* horizon_count,
+                         int32_t* parents, int32_t parents_cap, int32_t* n_nodes);
+
+/*
+ * Accepted-path cache extraction (the commit that follows acceptance in the
+ * step's timing, App. C paragraph "Metrics and timing"). For every layer l and trajectory b with
+ * n = out_len[b] - 1 accepted nodes, the K/V rows of the root (the anchor,
+ * node 0) and then of acc_nodes[b][0..n-1] are copied, bit for bit, to sequence
+ * positions ctx_len[b], ctx_len[b] + 1, ... of b's paged cache (position p is
+ * slot p % block_size of page block_table[b][p / block_size]), and
+ * new_ctx_len[b] = ctx_len[b] + out_len[b]. The terminal (fallback or bonus)
+ * token becomes the next round's anchor and has no K/V yet. Layers are stacked
+ * along the leading dimension, so one launch commits the whole model.
+ */
+typedef struct {
+  int32_t n_layers;      /* stacked layers, 1..65535                                   */
+  int32_t B, T;          /* trajectories; tree nodes (1..SR_MAX_TREE)                 */
+  int32_t Hkv, D;        /* KV heads; head dim with D * element size a multiple of 16 */
+  int32_t block_size;    /* tokens per KV page, >= 1                                  */
+  int32_t max_blocks;    /* columns of block_table, >= 1                              */
+  int32_t num_blocks;    /* pages per layer in k_cache / v_cache, >= 1                */
+  int32_t max_depth;     /* columns of acc_nodes, 0..SR_MAX_TREE                      */
+  sr_dtype dtype;        /* element type of the caches and tree K/V                   */
+} sr_commit_desc;
+
+/*
+ * acc_nodes   [B,max_depth]                          int32  accepted node ids in walk order (as
+ *                                                           sr_tree_accept writes them); may be NULL
+ *                                                           when max_depth == 0
+ * out_len     [B]                                    int32  1 + accepted count (as sr_tree_accept
+ *                                                           writes it; its invalid 0 is rejected here)
+ * parents     [B,T]                                  int32  (optional, NULL = not checked) topology;
+ *                                                           when given the nodes must form a root path
+ * k_tree      [n_layers,B,T,Hkv,D]                   dtype  keys of the tree tokens, every layer
+ * v_tree      [n_layers,B,T,Hkv,D]                   dtype  values of the tree tokens
+ * block_table [B,max_blocks]                         int32  physical page of logical page i
+ * ctx_len     [B]                                    int32  tokens already in the cache
+ * k_cache     [n_layers,num_blocks,Hkv,block_size,D] dtype  IN/OUT paged keys
+ * v_cache     [n_layers,num_blocks,Hkv,block_size,D] dtype  IN/OUT paged values
+ * new_ctx_len [B]                                    int32  OUT; -1 for a rejected trajectory
+ * Rejected trajectory (out_len outside [1, max_depth + 1]; a node id outside
+ * [1, T); a broken root path when parents is given; ctx_len < 0 or
+ * ctx_len + out_len > max_blocks * block_size; a page to write outside
+ * [0, num_blocks)): none of its cache rows is written. new_ctx_len must not
+ * overlap ctx_len; tree K/V must not overlap the caches; no two trajectories
+ * may write the same page slot (their writes would race). k_tree, v_tree and
+ * the caches must be 16-byte aligned.
+ */
+sr_status sr_commit_path(const sr_commit_desc* desc, const int32_t* acc_nodes, const int32_t* out_len,
+                         const int32_t* parents, const void* k_tree, const void* v_tree,
+                         const int32_t* block_table, const int32_t* ctx_len, void* k_cache, void* v_cache,
+                         int32_t* new_ctx_len, void* stream);
 
 /* ========================================================================== *
  * Kernel timing hook

@@ -13,7 +13,7 @@ from the paper (SpecRoll, arXiv 2608.04962):
                    residuals (App. B.2, Eq. (nodeaccept), Eq. (noderesidual),
                    Alg. "Exact node-wise tree verification").
 * ``engine``    -- the concurrency-aware node budget and the tree it allows
-                   (Sec. 3.3, Eq. (verification-budget), Eq. (tree-budget)) and
+                   (Sec. 3.2, Eq. (verification-budget), Eq. (tree-budget)) and
                    the accepted-path cache extraction.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of

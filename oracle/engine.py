@@ -1,9 +1,10 @@
 """Engine steps around the verification step (oracle; test infrastructure only).
 
-Paper: Sec. 3.3, Eq. (verification-budget) and Eq. (tree-budget); App. "Implementation and
+Paper: Sec. 3.2, Eq. (verification-budget) and Eq. (tree-budget); App. C "Implementation and
 Reproducibility Details", paragraph "Concurrency-aware sparse tree verification" (C_peak = 512,
 N_min = 1, N_max = 10, root counted, nominal non-root allocation (5, 4, 0) over the horizons,
-truncated to the budget); Sec. 5 timing list ("accepted-path cache extraction").
+truncated to the budget); App. C, paragraph "Metrics and timing" (accepted-path cache extraction is
+part of each step).
 
 Readings taken here (the paper leaves them open):
 * Truncation keeps the shallowest horizons first: horizon h receives min(n_h^nominal, what is left of

@@ -8,6 +8,9 @@ memory and the current stream.
     tree_build        the tree-build half on given head logits
     tree_verify_attn  tree-masked attention over the paged prefix (App. B.1 Eq. (nodep))
     tree_accept       exact node-wise acceptance walk      (App. B.2)
+    commit_path       accepted path's K/V appended to the paged cache, all layers in one launch
+    tree_budget       per-response node budget and its tree (Sec. 3.2 Eq. (verification-budget),
+                      Eq. (tree-budget)); host-only
 """
 from __future__ import annotations
 
@@ -18,9 +21,10 @@ from typing import Optional
 import torch
 
 from . import _lib
-from ._lib import AcceptDesc, AttnDesc, HeadsDesc, SpecRollError, check, lib  # noqa: F401
+from ._lib import AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, SpecRollError, check, lib  # noqa: F401
 
-__all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "prof_begin", "prof_end",
+__all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "commit_path", "tree_budget",
+           "prof_begin", "prof_end",
            "kernel_names", "version", "SpecRollError", "library_path"]
 
 _DT = {torch.float32: _lib.SR_F32, torch.bfloat16: _lib.SR_BF16}
@@ -216,6 +220,61 @@ def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, max_d
     if max_depth == 0:
         outputs["acc_nodes"] = outputs["acc_nodes"][:, :0]
     return outputs
+
+
+def tree_budget(live: int, c_peak: int = 512, n_min: int = 1, n_max: int = 10, alloc=(5, 4, 0)):
+    """Host rule of the node budget. Returns (N_t, per-horizon node counts, parents list of the tree)."""
+    al = (C.c_int32 * max(1, len(alloc)))(*[int(a) for a in alloc])
+    desc = BudgetDesc(int(c_peak), int(n_min), int(n_max), len(alloc), al)
+    cap = max(int(n_max), 1)
+    par = (C.c_int32 * cap)()
+    cnt = (C.c_int32 * max(1, len(alloc)))()
+    n_t, n_nodes = C.c_int32(), C.c_int32()
+    check(lib().sr_tree_budget(C.byref(desc), int(live), C.byref(n_t), cnt, par, cap, C.byref(n_nodes)),
+          "sr_tree_budget")
+    counts = [int(cnt[h]) for h in range(len(alloc))]
+    while counts and counts[-1] == 0:
+        counts.pop()
+    return int(n_t.value), counts, [int(par[i]) for i in range(n_nodes.value)]
+
+
+def commit_path(k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, acc_nodes, out_len, parents=None,
+                new_ctx_len=None):
+    """Append the root and accepted nodes' K/V rows to the paged caches (in place).
+
+    k_cache/v_cache [n_layers,NB,Hkv,bs,D] (or [NB,Hkv,bs,D] for one layer), k_tree/v_tree
+    [n_layers,B,T,Hkv,D] (or [B,T,Hkv,D]), block_table [B,max_blocks] int32, ctx_len [B] int32,
+    acc_nodes [B,max_depth] int32, out_len [B] int32, parents [B,T] int32 or None.
+    Returns new_ctx_len [B] int32 (-1 for a rejected trajectory)."""
+    dev = k_cache.device
+    one = k_cache.dim() == 4
+    kc = k_cache.unsqueeze(0) if one else k_cache
+    kt = k_tree.unsqueeze(0) if one else k_tree
+    nl, NB, Hkv, bs, D = kc.shape
+    _, B, T, _, _ = kt.shape
+    dt = k_cache.dtype
+    if dt not in _DT:
+        raise TypeError("caches must be float32 or bfloat16")
+    _need(k_cache, "k_cache", dt, tuple(k_cache.shape), dev)
+    _need(v_cache, "v_cache", dt, tuple(k_cache.shape), dev)
+    _need(k_tree, "k_tree", dt, ((B, T, Hkv, D) if one else (nl, B, T, Hkv, D)), dev)
+    _need(v_tree, "v_tree", dt, tuple(k_tree.shape), dev)
+    _need(block_table, "block_table", torch.int32, (B, block_table.shape[1]), dev)
+    _need(ctx_len, "ctx_len", torch.int32, (B,), dev)
+    _need(out_len, "out_len", torch.int32, (B,), dev)
+    max_depth = int(acc_nodes.shape[1])
+    _need(acc_nodes, "acc_nodes", torch.int32, (B, max_depth), dev)
+    if parents is not None:
+        _need(parents, "parents", torch.int32, (B, T), dev)
+    if new_ctx_len is None:
+        new_ctx_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    _need(new_ctx_len, "new_ctx_len", torch.int32, (B,), dev)
+    desc = CommitDesc(nl, B, T, Hkv, D, bs, block_table.shape[1], NB, max_depth, _DT[dt])
+    st = lib().sr_commit_path(C.byref(desc), _ptr(acc_nodes), _ptr(out_len), _ptr(parents), _ptr(k_tree),
+                              _ptr(v_tree), _ptr(block_table), _ptr(ctx_len), _ptr(k_cache), _ptr(v_cache),
+                              _ptr(new_ctx_len), _stream(dev))
+    check(st, "sr_commit_path")
+    return new_ctx_len
 
 
 def prof_begin(kernel_substr: str) -> None:

@@ -35,6 +35,17 @@ class AcceptDesc(C.Structure):
                 ("logit_dtype", C.c_int32), ("temperature", C.c_float)]
 
 
+class BudgetDesc(C.Structure):
+    _fields_ = [("c_peak", C.c_int32), ("n_min", C.c_int32), ("n_max", C.c_int32), ("n_alloc", C.c_int32),
+                ("alloc", _i32p)]
+
+
+class CommitDesc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("B", C.c_int32), ("T", C.c_int32), ("Hkv", C.c_int32),
+                ("D", C.c_int32), ("block_size", C.c_int32), ("max_blocks", C.c_int32),
+                ("num_blocks", C.c_int32), ("max_depth", C.c_int32), ("dtype", C.c_int32)]
+
+
 # name -> (restype, argtypes)
 SIGNATURES = {
     "sr_last_error": (C.c_char_p, []),
@@ -51,6 +62,8 @@ SIGNATURES = {
     "sr_tree_accept_workspace": (C.c_size_t, [C.POINTER(AcceptDesc)]),
     "sr_tree_accept": (C.c_int, [C.POINTER(AcceptDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                  C.c_size_t, _p]),
+    "sr_tree_budget": (C.c_int, [C.POINTER(BudgetDesc), C.c_int32, _i32p, _i32p, _i32p, C.c_int32, _i32p]),
+    "sr_commit_path": (C.c_int, [C.POINTER(CommitDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]),
     "sr_prof_begin": (C.c_int, [C.c_char_p]),
     "sr_prof_end": (C.c_int, [C.POINTER(C.c_double), _i32p]),
 }

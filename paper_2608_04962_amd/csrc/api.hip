@@ -145,7 +145,7 @@ const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
 
 const char* sr_kernel_names(void) {
   return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_tree_attn;"
-         "sr_attn_combine;sr_tree_accept";
+         "sr_attn_combine;sr_tree_accept;sr_commit_path";
 }
 
 // ------------------------------------------------------------------ proposal
@@ -287,6 +287,72 @@ sr_status sr_tree_accept(const sr_accept_desc* d, const void* target_logits, con
   SR_CHECK(aligned16(target_logits), "target_logits must be 16-byte aligned");
   return launch_tree_accept(*d, target_logits, child_logit, tokens, parents, u_acc, u_fin, acc_nodes, out_tokens,
                             out_len, final_kind, min_margin, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ engine glue
+sr_status sr_tree_budget(const sr_budget_desc* d, int32_t live, int32_t* n_t, int32_t* horizon_count,
+                         int32_t* parents, int32_t parents_cap, int32_t* n_nodes) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(n_t && parents && n_nodes, "a required pointer is null");
+  SR_CHECK(d->c_peak >= 1, "c_peak must be >= 1 (got %d)", d->c_peak);
+  SR_CHECK(d->n_min >= 1 && d->n_min <= d->n_max && d->n_max <= SR_MAX_TREE,
+           "need 1 <= n_min <= n_max <= %d (got %d, %d)", SR_MAX_TREE, d->n_min, d->n_max);
+  SR_CHECK(d->n_alloc >= 0 && d->n_alloc <= SR_MAX_TREE, "n_alloc must be in [0, %d]", SR_MAX_TREE);
+  SR_CHECK(d->n_alloc == 0 || d->alloc != nullptr, "alloc is null");
+  SR_CHECK(live >= 1, "live must be >= 1 (got %d)", live);
+  for (int h = 0; h < d->n_alloc; ++h) SR_CHECK(d->alloc[h] >= 0, "alloc[%d] is negative", h);
+  // Eq. (verification-budget): the per-response share of the capacity, clipped
+  const int32_t share = d->c_peak / live;
+  const int32_t budget = share < d->n_min ? d->n_min : (share > d->n_max ? d->n_max : share);
+  // Eq. (tree-budget): the anchor plus the horizons, filled shallowest first
+  int32_t cnt[SR_MAX_TREE];
+  int32_t used = 1, levels = 0;
+  for (int h = 0; h < d->n_alloc; ++h) {
+    const int32_t give = d->alloc[h] < budget - used ? d->alloc[h] : budget - used;
+    if (give <= 0) break;
+    cnt[levels++] = give;
+    used += give;
+  }
+  SR_CHECK(used <= parents_cap, "parents_cap %d cannot hold the %d-node tree", parents_cap, used);
+  parents[0] = -1;
+  int32_t prev_first = 0, prev_n = 1, next = 1;
+  for (int h = 0; h < levels; ++h) {
+    for (int32_t k = 0; k < cnt[h]; ++k) parents[next + k] = prev_first + (k * prev_n) / cnt[h];
+    prev_first = next;
+    prev_n = cnt[h];
+    next += cnt[h];
+  }
+  if (horizon_count)
+    for (int h = 0; h < d->n_alloc; ++h) horizon_count[h] = h < levels ? cnt[h] : 0;
+  *n_t = budget;
+  *n_nodes = used;
+  return SR_OK;
+}
+
+sr_status sr_commit_path(const sr_commit_desc* d, const int32_t* acc_nodes, const int32_t* out_len,
+                         const int32_t* parents, const void* k_tree, const void* v_tree, const int32_t* block_table,
+                         const int32_t* ctx_len, void* k_cache, void* v_cache, int32_t* new_ctx_len, void* stream) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(d->n_layers >= 1 && d->n_layers <= 65535, "n_layers must be in [1, 65535] (got %d)", d->n_layers);
+  SR_CHECK(d->B >= 1, "B must be >= 1 (got %d)", d->B);
+  SR_CHECK(d->T >= 1 && d->T <= SR_MAX_TREE, "T must be in [1, %d] (got %d)", SR_MAX_TREE, d->T);
+  SR_CHECK(d->Hkv >= 1 && d->D >= 1, "Hkv and D must be >= 1");
+  SR_CHECK(dtype_ok(d->dtype), "unknown dtype %d", (int)d->dtype);
+  SR_CHECK(((size_t)d->D * esize(d->dtype)) % 16 == 0, "D * element size must be a multiple of 16 bytes (D = %d)",
+           d->D);
+  SR_CHECK(d->block_size >= 1 && d->max_blocks >= 1 && d->num_blocks >= 1,
+           "block_size, max_blocks and num_blocks must be >= 1");
+  SR_CHECK((size_t)d->max_blocks * d->block_size <= (size_t)INT32_MAX / 2, "max_blocks * block_size too large");
+  SR_CHECK(d->max_depth >= 0 && d->max_depth <= SR_MAX_TREE, "max_depth must be in [0, %d]", SR_MAX_TREE);
+  SR_CHECK((size_t)2 * (d->max_depth + 1) * d->Hkv * d->D <= (size_t)INT32_MAX / 4, "Hkv * D too large");
+  SR_CHECK(out_len && k_tree && v_tree && block_table && ctx_len && k_cache && v_cache && new_ctx_len,
+           "a required pointer is null");
+  SR_CHECK(d->max_depth == 0 || acc_nodes != nullptr, "acc_nodes is null");
+  SR_CHECK(aligned16(k_tree) && aligned16(v_tree) && aligned16(k_cache) && aligned16(v_cache),
+           "tree K/V and caches must be 16-byte aligned");
+  SR_CHECK(new_ctx_len != ctx_len, "new_ctx_len must not overlap ctx_len");
+  return launch_commit_path(*d, acc_nodes, out_len, parents, k_tree, v_tree, block_table, ctx_len, k_cache, v_cache,
+                            new_ctx_len, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ timing hook

@@ -38,4 +38,10 @@ sr_status launch_tree_accept(const sr_accept_desc& d, const void* target_logits,
                              const float* u_fin, int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len,
                              uint8_t* final_kind, float* min_margin, hipStream_t s);
 
+// ---- engine glue (k_engine.hip)
+sr_status launch_commit_path(const sr_commit_desc& d, const int32_t* acc_nodes, const int32_t* out_len,
+                             const int32_t* parents, const void* k_tree, const void* v_tree,
+                             const int32_t* block_table, const int32_t* ctx_len, void* k_cache, void* v_cache,
+                             int32_t* new_ctx_len, hipStream_t s);
+
 }  // namespace sr

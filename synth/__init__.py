@@ -364,14 +364,15 @@ def accept_inputs(cfg: Config, seed: int = 0, target_std: float = 4.0, noise_std
     )
 
 
-def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1) -> dict:
+def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1, with_kv: bool = True) -> dict:
     """Inputs of the accepted-path cache extraction, stacked over ``n_layers`` layers.
 
     Each trajectory's page list has room for its prefix plus a full root path (depth + 1 rows).
     The accepted path is a random root path of a random target length 0..depth (at every step a
     uniformly chosen child among those whose subtree reaches that length, else among all children,
     stopping early at a leaf); out_len = 1 + its length. Cache slots past the prefix hold
-    NaN, so a row that is not written stays visibly untouched.
+    NaN, so a row that is not written stays visibly untouched. ``with_kv=False`` skips the cache and
+    tree K/V draws (page lists, lengths and paths only).
     """
     B, T, Hkv, D, bs = cfg.B, cfg.T, cfg.Hkv, cfg.D, cfg.block_size
     par = topology(cfg)
@@ -388,12 +389,13 @@ def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1) -> dict:
     for b in range(B):
         table[b, :nblk[b]] = phys[off:off + nblk[b]]
         off += nblk[b]
-    kc = normal(_rng(seed, cfg, "ckc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
-    vc = normal(_rng(seed, cfg, "cvc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
-    for b in range(B):
-        pos = np.arange(int(L[b]), int(nblk[b]) * bs)
-        kc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
-        vc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
+    if with_kv:
+        kc = normal(_rng(seed, cfg, "ckc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
+        vc = normal(_rng(seed, cfg, "cvc"), (n_layers, num_blocks, Hkv, bs, D), 1.0)
+        for b in range(B):
+            pos = np.arange(int(L[b]), int(nblk[b]) * bs)
+            kc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
+            vc[:, table[b, pos // bs], :, pos % bs, :] = np.nan
     kids = [[] for _ in range(T)]
     for c in range(1, T):
         kids[par[c]].append(c)
@@ -413,12 +415,15 @@ def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1) -> dict:
             acc[b, n] = u
             n += 1
         out_len[b] = n + 1
-    return dict(
+    out = dict(
         cfg=cfg, dtype=cfg.dtype, n_layers=n_layers, ctx_len=L.astype(np.int32), block_table=table,
         num_blocks=num_blocks, max_blocks=max_blocks, max_depth=max(1, max_depth),
-        k_cache=as_dtype(kc, cfg.dtype), v_cache=as_dtype(vc, cfg.dtype),
-        k_tree=as_dtype(normal(_rng(seed, cfg, "ckt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
-        v_tree=as_dtype(normal(_rng(seed, cfg, "cvt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
         parents=np.ascontiguousarray(np.broadcast_to(par, (B, T))).astype(np.int32),
         acc_nodes=acc, out_len=out_len,
     )
+    if with_kv:
+        out.update(
+            k_cache=as_dtype(kc, cfg.dtype), v_cache=as_dtype(vc, cfg.dtype),
+            k_tree=as_dtype(normal(_rng(seed, cfg, "ckt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
+            v_tree=as_dtype(normal(_rng(seed, cfg, "cvt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype))
+    return out

@@ -37,6 +37,8 @@ def test_struct_layouts_match_header():
     assert C.sizeof(_lib.HeadsDesc) == 9 * 4
     assert C.sizeof(_lib.AttnDesc) == 10 * 4
     assert C.sizeof(_lib.AcceptDesc) == 6 * 4
+    assert C.sizeof(_lib.CommitDesc) == 10 * 4
+    assert C.sizeof(_lib.BudgetDesc) == 4 * 4 + C.sizeof(C.c_void_p)
 
 
 def _call_heads(desc, **ptrs):
@@ -102,3 +104,60 @@ def test_workspace_queries_are_consistent():
 def test_prof_hook_host_side():
     _lib.check(_lib.lib().sr_prof_begin(b"sr_tree_attn"), "begin")
     assert sr.prof_end() == (0.0, 0)
+
+
+@pytest.mark.parametrize("field,value", [("n_layers", 0), ("n_layers", 70000), ("B", 0), ("T", 0), ("T", 129),
+                                         ("D", 4), ("dtype", 5), ("block_size", 0), ("max_depth", -1),
+                                         ("max_depth", 200), ("num_blocks", 0)])
+def test_commit_descriptor_rejected(field, value):
+    desc = _lib.CommitDesc(2, 4, 8, 2, 64, 16, 10, 40, 3, _lib.SR_BF16)
+    setattr(desc, field, value)
+    fake = C.c_void_p(1 << 20)    # never dereferenced: the descriptor check fails first
+    st = _lib.lib().sr_commit_path(C.byref(desc), *([fake] * 10), None)
+    assert st == _lib.SR_ERR_INVALID
+    assert _lib.last_error()
+
+
+def test_commit_pointer_checks():
+    desc = _lib.CommitDesc(2, 4, 8, 2, 64, 16, 10, 40, 3, _lib.SR_BF16)
+    fake = C.c_void_p(1 << 20)
+    args = [fake] * 10
+    args[0] = None                                      # acc_nodes with max_depth > 0
+    assert _lib.lib().sr_commit_path(C.byref(desc), *args, None) == _lib.SR_ERR_INVALID
+    args = [fake] * 10
+    args[3] = C.c_void_p((1 << 20) + 8)                 # misaligned k_tree
+    assert _lib.lib().sr_commit_path(C.byref(desc), *args, None) == _lib.SR_ERR_INVALID
+    args = [fake] * 10
+    args[9] = args[6]                                   # new_ctx_len == ctx_len
+    assert _lib.lib().sr_commit_path(C.byref(desc), *args, None) == _lib.SR_ERR_INVALID
+    assert "overlap" in _lib.last_error()
+
+
+@pytest.mark.parametrize("c_peak,n_min,n_max,alloc", [
+    (512, 1, 10, (5, 4, 0)), (300, 3, 17, (1, 6, 2, 9)), (64, 1, 5, (0, 3)), (7, 1, 128, (100, 100)), (50, 2, 9, ())])
+def test_tree_budget_host_rule_matches_oracle(c_peak, n_min, n_max, alloc):
+    """sr_tree_budget is host-only integer logic, so its parity with the oracle runs here, bit-exact."""
+    import oracle
+    for live in list(range(1, 2 * c_peak + 3)) + [10 ** 6]:
+        got = sr.tree_budget(live, c_peak, n_min, n_max, alloc)
+        n_t, counts, parents = oracle.tree_budget(live, c_peak, n_min, n_max, alloc)
+        assert got == (n_t, counts, parents.tolist()), live
+
+
+def test_tree_budget_rejections():
+    lib = _lib.lib()
+    al = (C.c_int32 * 3)(5, 4, 0)
+    out = [C.c_int32() for _ in range(2)]
+    par = (C.c_int32 * 10)()
+    good = _lib.BudgetDesc(512, 1, 10, 3, al)
+    args = lambda live, cap: (live, C.byref(out[0]), None, par, cap, C.byref(out[1]))  # noqa: E731
+    assert lib.sr_tree_budget(C.byref(good), *args(1, 10)) == _lib.SR_OK
+    assert (out[0].value, out[1].value) == (10, 10)
+    assert lib.sr_tree_budget(C.byref(good), *args(0, 10)) == _lib.SR_ERR_INVALID
+    assert lib.sr_tree_budget(C.byref(good), *args(1, 9)) == _lib.SR_ERR_INVALID     # capacity below the tree
+    assert lib.sr_tree_budget(C.byref(good), *args(200, 3)) == _lib.SR_OK             # 512 // 200 = 2 nodes
+    assert (out[0].value, out[1].value) == (2, 2) and par[:2] == [-1, 0]
+    for bad in (_lib.BudgetDesc(0, 1, 10, 3, al), _lib.BudgetDesc(512, 0, 10, 3, al),
+                _lib.BudgetDesc(512, 4, 3, 3, al), _lib.BudgetDesc(512, 1, 129, 3, al),
+                _lib.BudgetDesc(512, 1, 10, 3, None), _lib.BudgetDesc(512, 1, 10, 2, (C.c_int32 * 2)(3, -1))):
+        assert lib.sr_tree_budget(C.byref(bad), *args(1, 200)) == _lib.SR_ERR_INVALID

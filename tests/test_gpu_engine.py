@@ -1,0 +1,153 @@
+"""GPU parity of sr_commit_path (accepted-path cache extraction) against the oracle: bit-exact caches and
+lengths on seeded inputs from the tiny case to the 7B shape at full size, stacked layers, the rejection
+rules, and the acceptance walk feeding the commit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_04962_amd as sr
+import synth
+from helpers import dev_tensor
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    """Raw stored bits of a device tensor (NaN-safe exact comparison)."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.view(torch.int32).cpu().numpy().view(np.uint32)
+
+
+def _raw(x: np.ndarray) -> np.ndarray:
+    return x if x.dtype == np.uint16 else x.view(np.uint32)
+
+
+def _gpu_commit(inp, parents=True, acc=None, out_len=None, ctx=None, table=None):
+    dv = {k: dev_tensor(inp[k]) for k in ("k_cache", "v_cache", "k_tree", "v_tree")}
+    table = inp["block_table"] if table is None else table
+    ctx = inp["ctx_len"] if ctx is None else ctx
+    acc = inp["acc_nodes"] if acc is None else acc
+    out_len = inp["out_len"] if out_len is None else out_len
+    new = sr.commit_path(dv["k_cache"], dv["v_cache"], dev_tensor(table), dev_tensor(ctx), dv["k_tree"],
+                         dv["v_tree"], dev_tensor(acc), dev_tensor(out_len),
+                         parents=dev_tensor(inp["parents"]) if parents else None)
+    torch.cuda.synchronize()
+    return _bits(dv["k_cache"]), _bits(dv["v_cache"]), new.cpu().numpy()
+
+
+def _oracle_commit(inp, rows, acc=None, out_len=None, ctx=None, table=None):
+    """Expected caches when only ``rows`` commit (the others are rejected and leave no trace)."""
+    table = inp["block_table"] if table is None else table
+    ctx = inp["ctx_len"] if ctx is None else ctx
+    acc = inp["acc_nodes"] if acc is None else acc
+    out_len = inp["out_len"] if out_len is None else out_len
+    rows = np.asarray(rows, dtype=np.int64)
+    ks, vs = [], []
+    new = np.full(inp["cfg"].B, -1, dtype=np.int32)
+    for l in range(inp["n_layers"]):
+        k, v, n = oracle.commit_path(_raw(inp["k_cache"][l]), _raw(inp["v_cache"][l]), table[rows], ctx[rows],
+                                     _raw(inp["k_tree"][l])[rows], _raw(inp["v_tree"][l])[rows], acc[rows],
+                                     out_len[rows], inp["cfg"].block_size)
+        ks.append(k)
+        vs.append(v)
+        new[rows] = n
+    return np.stack(ks), np.stack(vs), new
+
+
+def _check(inp, parents=True):
+    cfg = inp["cfg"]
+    print(f"[commit] {cfg.name} B={cfg.B} T={cfg.T} layers={inp['n_layers']} dtype={cfg.dtype}", flush=True)
+    gk, gv, gn = _gpu_commit(inp, parents)
+    ek, ev, en = _oracle_commit(inp, range(cfg.B))
+    np.testing.assert_array_equal(gn, en)
+    assert np.array_equal(gk, ek) and np.array_equal(gv, ev)
+
+
+CASES = {
+    "tiny-fp32": (synth.CONFIGS[0], 1),
+    "1.5B-shape-2-layers": (synth.scaled(synth.CONFIGS[1], ctx=("uniform", 1, 700)), 2),
+    "14B-tail-3-layers": (synth.scaled(synth.CONFIGS[3], ctx=("uniform", 100, 900)), 3),
+    "7B-sweep-B4-T96": (synth.scaled(synth.sweep_config(4, 96), ctx=("uniform", 1, 300)), 2),
+    "7B-shape-9-layers": (synth.scaled(synth.CONFIGS[2], B=16, ctx=("uniform", 1, 200)), 9),
+    "fp32-D64-ragged": (synth.scaled(synth.CONFIGS[0], B=33, T=24, depth=4, parents=None,
+                                     ctx=("uniform", 0, 50), contiguous_pages=False), 1),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("parents", [True, False])
+def test_commit_parity(name, parents):
+    cfg, nl = CASES[name]
+    _check(synth.commit_inputs(cfg, seed=1, n_layers=nl), parents)
+
+
+def test_commit_full_size_7b():
+    """Full 7B-shape step: B=128, contexts uniform in [1024, 8192], one layer of the stacked layout."""
+    _check(synth.commit_inputs(synth.CONFIGS[2], seed=2, n_layers=1))
+
+
+def test_commit_rejections():
+    cfg = synth.scaled(synth.CONFIGS[2], B=10, ctx=("uniform", 20, 100))
+    inp = synth.commit_inputs(cfg, seed=4, n_layers=2)
+    acc = inp["acc_nodes"].copy()
+    out_len = inp["out_len"].copy()
+    ctx = inp["ctx_len"].copy()
+    table = inp["block_table"].copy()
+    md = inp["max_depth"]
+    par = inp["parents"][0]
+    bs = cfg.block_size
+    deep = [c for c in range(1, cfg.T) if par[c] != 0][0]          # a node whose parent is not the root
+    # 0: acceptance's invalid marker; 1: longer than max_depth + 1; 2: node id out of range;
+    # 3: not a root path (rejected only when parents is given); 4: no room in the page list;
+    # 5: a page to write outside [0, num_blocks); 6: negative context; 7: page id -1; 8, 9: valid
+    out_len[0] = 0
+    out_len[1] = md + 2
+    out_len[2] = 3
+    acc[2, :2] = [1, cfg.T]
+    out_len[3] = 2
+    acc[3, 0] = deep
+    ctx[4] = table.shape[1] * bs - out_len[4] + 1
+    table[5, ctx[5] // bs] = inp["num_blocks"]
+    ctx[6] = -1
+    table[7, (ctx[7] + out_len[7] - 1) // bs] = -1
+    gk, gv, gn = _gpu_commit(inp, True, acc, out_len, ctx, table)
+    ek, ev, en = _oracle_commit(inp, [8, 9], acc, out_len, ctx, table)
+    np.testing.assert_array_equal(gn, en)
+    assert (gn[:8] == -1).all()
+    assert np.array_equal(gk, ek) and np.array_equal(gv, ev)
+    # without the topology the non-path case 3 commits its rows as given
+    gk, gv, gn = _gpu_commit(inp, False, acc, out_len, ctx, table)
+    ek, ev, en = _oracle_commit(inp, [3, 8, 9], acc, out_len, ctx, table)
+    np.testing.assert_array_equal(gn, en)
+    assert np.array_equal(gk, ek) and np.array_equal(gv, ev)
+
+
+def test_accept_then_commit():
+    """sr_tree_accept's outputs feed sr_commit_path directly; the oracle runs its own walk and commit."""
+    cfg = synth.scaled(synth.CONFIGS[0], B=48, ctx=("uniform", 0, 120))
+    ai = synth.accept_inputs(cfg, seed=7)
+    ci = synth.commit_inputs(cfg, seed=7, n_layers=2)
+    res = sr.tree_accept(dev_tensor(ai["target_logits"]), dev_tensor(ai["child_logit"]), dev_tensor(ai["tokens"]),
+                         dev_tensor(ai["parents"]), dev_tensor(ai["u_acc"]), dev_tensor(ai["u_fin"]),
+                         ai["max_depth"], 1.0)
+    o = oracle.tree_accept(synth.to_f64(ai["target_logits"], cfg.dtype), ai["child_logit"], ai["tokens"],
+                           ai["parents"], ai["u_acc"], ai["u_fin"], 1.0, ai["max_depth"])
+    dv = {k: dev_tensor(ci[k]) for k in ("k_cache", "v_cache", "k_tree", "v_tree")}
+    new = sr.commit_path(dv["k_cache"], dv["v_cache"], dev_tensor(ci["block_table"]), dev_tensor(ci["ctx_len"]),
+                         dv["k_tree"], dv["v_tree"], res["acc_nodes"], res["out_len"],
+                         parents=dev_tensor(ai["parents"]))
+    torch.cuda.synchronize()
+    g_len = res["out_len"].cpu().numpy()
+    same = [b for b in range(cfg.B) if g_len[b] == o["out_len"][b]
+            and np.array_equal(res["acc_nodes"].cpu().numpy()[b], o["acc_nodes"][b])]
+    assert len(same) >= cfg.B - 1
+    ek, ev, en = _oracle_commit(ci, same, acc=o["acc_nodes"], out_len=o["out_len"].astype(np.int32))
+    gk, gv, gn = _bits(dv["k_cache"]), _bits(dv["v_cache"]), new.cpu().numpy()
+    np.testing.assert_array_equal(gn[same], en[same])
+    bs = cfg.block_size
+    for b in same:
+        for p in range(-(-int(en[b]) // bs)):
+            pg = ci["block_table"][b, p]
+            assert np.array_equal(gk[:, pg], ek[:, pg]) and np.array_equal(gv[:, pg], ev[:, pg])

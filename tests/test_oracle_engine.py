@@ -1,5 +1,5 @@
-"""Pins of the engine-glue oracle: the concurrency-aware node budget (Sec. 3.3, Eq. (verification-budget),
-Eq. (tree-budget); App. "Implementation and Reproducibility Details", paragraph "Concurrency-aware sparse
+"""Pins of the engine-glue oracle: the concurrency-aware node budget (Sec. 3.2, Eq. (verification-budget),
+Eq. (tree-budget); App. C "Implementation and Reproducibility Details", paragraph "Concurrency-aware sparse
 tree verification") and the accepted-path cache extraction."""
 import numpy as np
 import pytest
