@@ -4,8 +4,10 @@ A step is the whole hot path over one batch of synthetic inputs resident in HBM:
   sr_heads_propose (heads + vocabulary projection + draft tree)
   -> sr_tree_verify_attn (tree-masked attention over the paged prefix, one layer)
   -> sr_tree_accept (exact acceptance walk).
-After the timed steps, the accepted-path cache commit (sr_commit_path) of the last step's accepted
-paths is timed on its own for all 28 layers of the 7B-shaped target and reported beside the step.
+After the timed steps, two calls around the step are timed on their own and reported beside it: the
+accepted-path cache commit (sr_commit_path) of the last step's accepted paths for all 28 layers of the
+7B-shaped target, and the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
+horizon) slot on the step's own target-logit rows, head logits and draft trees.
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
 hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
 
@@ -31,7 +33,8 @@ CALIB_ELEMS = 1 << 28          # 1 GiB of float32 read and 1 GiB written by the 
 KERNEL_SOURCE = {"sr_tree_attn": "k_attn.hip", "sr_attn_combine": "k_attn.hip", "sr_vocab_gemm": "k_heads.hip",
                  "sr_head_gemm": "k_heads.hip", "sr_clip_ln": "k_heads.hip", "sr_group_max": "k_heads.hip",
                  "sr_topm": "k_heads.hip", "sr_topm_full": "k_heads.hip", "sr_tree_build": "k_heads.hip",
-                 "sr_tree_accept": "k_accept.hip", "sr_commit_path": "k_engine.hip"}
+                 "sr_tree_accept": "k_accept.hip", "sr_commit_path": "k_engine.hip",
+                 "sr_reflex_feedback": "k_reflex.hip"}
 COMMIT_LAYERS = 28             # decoder layers of the 7B-shaped target: one commit launch covers all of them
 
 
@@ -196,6 +199,7 @@ def main():
     }
 
     res["commit_path"] = commit_bench(sr, synth, cfg, args.seed, outs, dev)
+    res["reflex_feedback"] = reflex_bench(sr, cfg, H, C_, hin, hws, dev)
     res["tree_budget"] = dict(zip(("N_t", "horizon_counts", "parents"), sr.tree_budget(B)))
 
     if not args.no_cpu_baseline:
@@ -236,6 +240,69 @@ def commit_bench(sr, synth, cfg, seed, outs, dev):
     torch.cuda.empty_cache()
     return {"layers": nl, "rows_per_layer": rows, "avg_ms": avg, "launches": n, "algorithmic_bytes": alg,
             "GB/s": alg / (avg / 1e3) / 1e9, "frac_hbm_peak": alg / (avg / 1e3) / 1e9 / HBM_PEAK_GBPS}
+
+
+def reflex_bench(sr, cfg, H, C_, hin, hws, dev):
+    """Time sr_reflex_feedback for B*H records: record (i, h) takes trajectory i's target row at its first
+    depth-h node, the step's head-h logits of trajectory i, and the tokens of trajectory i's depth-h nodes
+    as candidates (the realised token is the first of them)."""
+    import numpy as np
+    import torch
+    B, T, Hh, V, d = cfg.B, cfg.T, cfg.H, cfg.V, cfg.d
+    logits = torch.empty((B, Hh, V), dtype=torch.float32, device=dev)
+    tok = torch.empty((B, T), dtype=torch.int32, device=dev)
+    cl = torch.empty((B, T), dtype=torch.float32, device=dev)
+    sr.heads_propose(H["hidden"], H["corr"], H["active"], H["A"], H["bias"], H["W"], H["parents"], H["root_token"],
+                     H["u_tree"], hin["max_children"], logits=logits, tokens=tok, child_logit=cl, workspace=hws)
+    torch.cuda.synchronize()
+    par = hin["parents"][0]
+    depth = np.zeros(T, dtype=np.int64)
+    for c in range(1, T):
+        depth[c] = depth[par[c]] + 1
+    by_depth = [np.nonzero(depth == h)[0] for h in range(Hh + 1)]
+    maxc = max(len(by_depth[h]) for h in range(1, Hh + 1))
+    tk = tok.cpu().numpy()
+    R = B * Hh
+    cand = np.full((R, maxc), -1, dtype=np.int32)
+    p_row = np.empty(R, dtype=np.int32)
+    q_row = np.empty(R, dtype=np.int32)
+    traj = np.empty(R, dtype=np.int32)
+    hor = np.empty(R, dtype=np.int32)
+    for i in range(B):
+        for h in range(1, Hh + 1):
+            r = i * Hh + h - 1
+            nodes = by_depth[h]
+            # distinct tokens of the depth-h nodes, in node order
+            seen = []
+            for u in nodes:
+                if int(tk[i, u]) not in seen:
+                    seen.append(int(tk[i, u]))
+            cand[r, :len(seen)] = seen
+            p_row[r] = i * T + int(nodes[0])
+            q_row[r] = i * Hh + h - 1
+            traj[r], hor[r] = i, h
+    t = lambda x: torch.from_numpy(x).to(dev)  # noqa: E731
+    args = (C_["target_logits"].view(B * T, V), t(p_row), logits.view(B * Hh, V), t(q_row), t(cand),
+            t(cand[:, 0].copy()), t(traj), t(hor), H["W"])
+    mem = torch.zeros((B, Hh, d), dtype=torch.float32, device=dev)
+    stats = torch.empty((R, 8), dtype=torch.float32, device=dev)
+    for _ in range(3):
+        sr.reflex_feedback(*args, mem, stats=stats)
+    torch.cuda.synchronize()
+    sr.prof_begin("sr_reflex_feedback")
+    for _ in range(20):
+        sr.reflex_feedback(*args, mem, stats=stats)
+    ms, n = sr.prof_end()
+    st = stats.cpu().numpy()
+    assert (st[:, 5] >= 0).all(), "invalid records in the feedback benchmark"
+    nS = float(st[:, 4].mean())
+    # per record: one target row (bf16), one head row (fp32), the support's rows of W, the memory row in/out
+    alg = R * (V * 2 + V * 4 + nS * d * 2 + 2 * d * 4)
+    avg = ms / max(n, 1)
+    del logits
+    return {"records": R, "mean_support": nS, "avg_ms": avg, "launches": n, "algorithmic_bytes": alg,
+            "GB/s": alg / (avg / 1e3) / 1e9, "frac_hbm_peak": alg / (avg / 1e3) / 1e9 / HBM_PEAK_GBPS,
+            "applied_frac": float((st[:, 5] == 1).mean())}
 
 
 def measured_traffic(kernel):

@@ -19,6 +19,9 @@
  *      sr_tree_budget       host rule for the per-response node budget and the
  *                           tree it allows (Sec. 3.2 Eq. (verification-budget),
  *                           Eq. (tree-budget)).
+ *   5. sr_reflex_feedback   verifier feedback of matured proposals folded into the
+ *                           trajectory-local Reflex memory (Sec. 3.3; Sec. 3.4
+ *                           Eq. (support) to Eq. (ema)).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -324,6 +327,81 @@ sr_status sr_commit_path(const sr_commit_desc* desc, const int32_t* acc_nodes, c
                          const int32_t* parents, const void* k_tree, const void* v_tree,
                          const int32_t* block_table, const int32_t* ctx_len, void* k_cache, void* v_cache,
                          int32_t* new_ctx_len, void* stream);
+
+/* ========================================================================== *
+ * 5. Reflex verifier feedback and memory update
+ * ========================================================================== *
+ * For every matured proposal record r (trajectory i, horizon h, candidate set C
+ * of K tokens, realised target token y*), with p = softmax(target logits /
+ * temperature) and q = softmax(head logits / temperature) over the whole
+ * vocabulary (Sec. 3.3 Eq. (conditional-distributions) to
+ * Eq. (acceptance-gap-decomposition); Sec. 3.4):
+ *   d_dist = p(C) TV(p_C, q_C),   d_cov = p(Top_K(p)) - p(C)
+ *   S      = C, then Top_K(p), then y*, then alternately the next token of
+ *            Top_k(p) and of Top_k(q), duplicates skipped, at most k = support
+ *            entries; top lists ordered by (logit desc, id asc)      Eq. (support)
+ *   r_dist = sum_{v in S} (p_S(v) - q_S(v)) W_v                       Eq. (distdir)
+ *   r_cov  = sum_{y in O} p_S(y) (W_y - mean_{b in B} W_b), O = Top_K(p) \ C,
+ *            B = the n_boundary candidates of lowest head logit (ties to the lower
+ *            id)                                                      Eq. (covdir)
+ *   g      = w_dist d_dist r_dist / (RMS(r_dist) + eps)
+ *          + w_cov d_cov r_cov / (RMS(r_cov) + eps)
+ *   e      = (d_dist + d_cov) g / (RMS(g) + eps)               Eq. (unified-feedback)
+ *   w      = clip(sev_tv TV(p_S, q_S) + sev_out (1 - p(C)), 0, 1)
+ * and if w >= w_min: memory[i][h-1] <- rho[h-1] memory[i][h-1] + (1 - rho[h-1]) e
+ * (Eq. (ema)). The paper's settings (App. C, "Verifier-derived feedback";
+ * Tab. "reflex-hparams") are support 48, w_dist 0.15, w_cov 1.25, sev_tv 0.3,
+ * sev_out 0.7, w_min 0.03, n_boundary 4, rho (.85, .90, .95). Exponentials are
+ * fp32, sums and the per-record scalars float64, the d-vectors fp32.
+ */
+typedef struct {
+  int32_t R;             /* records, >= 1                                          */
+  int32_t V, d;          /* vocabulary (multiple of 8, <= 262144); hidden size of W
+                            (multiple of 8, <= 8192)                               */
+  int32_t B, H;          /* memory slots [B,H,d]; H <= 8                           */
+  int32_t n_p_rows;      /* rows of target_logits                                  */
+  int32_t n_q_rows;      /* rows of head_logits                                    */
+  int32_t max_cand;      /* columns of cand, 1..support                            */
+  int32_t support;       /* support budget k, 1..64, <= V                          */
+  int32_t n_boundary;    /* boundary tokens, >= 1                                  */
+  sr_dtype p_dtype;      /* element type of target_logits                          */
+  sr_dtype w_dtype;      /* element type of W                                      */
+  float temperature;     /* > 0                                                    */
+  float w_dist, w_cov;   /* direction weights, >= 0                                */
+  float sev_tv, sev_out; /* severity coefficients                                  */
+  float w_min;           /* severity gate                                          */
+  float eps;             /* RMS stabiliser, > 0                                    */
+  float rho[8];          /* per-horizon decay in [0, 1), entries 0..H-1 used       */
+} sr_reflex_desc;
+
+/*
+ * target_logits [n_p_rows,V]  p_dtype  target logit rows (any rows; p_row picks one per record)
+ * p_row         [R]           int32    row of target_logits holding record r's target logits
+ * head_logits   [n_q_rows,V]  fp32     proposal (head) logit rows
+ * q_row         [R]           int32    row of head_logits holding record r's head logits
+ * cand          [R,max_cand]  int32    candidate ids, distinct, in slot order, then -1 padding
+ * y_star        [R]           int32    realised target token
+ * traj          [R]           int32    trajectory i in [0, B)
+ * horizon       [R]           int32    h in [1, H]
+ * W             [V,d]         w_dtype  the shared output projection (row = token)
+ * memory        [B,H,d]       fp32     IN/OUT Reflex memory m
+ * stats         [R,8]         fp32     OUT d_dist, d_cov, TV(p_S,q_S), w, |S|, applied, p(C),
+ *                                      p(Top_K(p)); applied = 1 (memory updated), 0 (w < w_min),
+ *                                      -1 (an earlier record of the call has the same (i, h): skipped,
+ *                                      so one call applies at most one record per slot, the first),
+ *                                      -2 (invalid record); the other entries are NaN for -1 and -2
+ * e_out         [R,d]         fp32     OUT (optional, NULL = not written) the feedback vector e
+ *                                      (NaN rows for skipped and invalid records)
+ * Invalid record: a row index, trajectory, horizon, y* or candidate id out of
+ * range, duplicate candidates, a candidate after a -1, or no candidate.
+ * Records are independent blocks; memory rows of distinct (i, h) are written by
+ * distinct records only. target_logits, head_logits and W must be 16-byte
+ * aligned.
+ */
+sr_status sr_reflex_feedback(const sr_reflex_desc* desc, const void* target_logits, const int32_t* p_row,
+                             const float* head_logits, const int32_t* q_row, const int32_t* cand,
+                             const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
+                             float* memory, float* stats, float* e_out, void* stream);
 
 /* ========================================================================== *
  * Kernel timing hook

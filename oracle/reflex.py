@@ -88,15 +88,15 @@ def feedback(p_logits: np.ndarray, q_logits: np.ndarray, cand: Sequence[int], y_
     pS = p[S] / p[S].sum()
     qS = q[S] / q[S].sum()
     tv_s = 0.5 * np.abs(pS - qS).sum()
-    Wd = np.asarray(W, dtype=np.float64)
-    r_dist = Wd[S].T @ (pS - qS)
+    W_S = np.asarray(W[S], dtype=np.float64)                  # rows of W are read as needed
+    r_dist = W_S.T @ (pS - qS)
     by_q = sorted(C, key=lambda c: (q[c], c))
     Bset = by_q[:n_boundary]
-    W_B = Wd[Bset].mean(axis=0)
+    W_B = np.asarray(W[Bset], dtype=np.float64).mean(axis=0)
     O = [int(y) for y in top_p[:K] if int(y) not in C and int(y) in S]
-    r_cov = np.zeros(Wd.shape[1])
+    r_cov = np.zeros(W_S.shape[1])
     for y in O:
-        r_cov += pS[S.index(y)] * (Wd[y] - W_B)
+        r_cov += pS[S.index(y)] * (W_S[S.index(y)] - W_B)
     rbar_dist = r_dist / (rms(r_dist) + eps)
     rbar_cov = r_cov / (rms(r_cov) + eps)
     g = w_dist * d_dist * rbar_dist + w_cov * d_cov * rbar_cov
@@ -113,10 +113,11 @@ def ema_update(m: np.ndarray, e: np.ndarray, rho: float) -> np.ndarray:
 
 def reflex_feedback(p_rows: np.ndarray, p_row: np.ndarray, q_rows: np.ndarray, q_row: np.ndarray,
                     cand: np.ndarray, y_star: np.ndarray, traj: np.ndarray, horizon: np.ndarray, W: np.ndarray,
-                    memory: np.ndarray, rho: Sequence[float], w_min: float = 0.03, **kw):
+                    memory: np.ndarray, rho: Sequence[float], w_min: float = 0.03, rows=None, **kw):
     """Batched records with the library's layout: cand [R, max_cand] (-1 padded), horizon 1-based,
     memory [B, H, d]. Records are applied in order; a record whose (trajectory, horizon) slot was already
-    used by an earlier record of the batch is skipped (applied = -1). Returns (new memory, list of dicts)."""
+    used by an earlier record of the batch is skipped (applied = -1). ``rows`` restricts the computation
+    to those records (the others are reported as None). Returns (new memory, list of dicts)."""
     mem = np.array(memory, dtype=np.float64, copy=True)
     seen = set()
     out = []
@@ -126,6 +127,9 @@ def reflex_feedback(p_rows: np.ndarray, p_row: np.ndarray, q_rows: np.ndarray, q
             out.append(dict(applied=-1))
             continue
         seen.add(slot)
+        if rows is not None and r not in rows:
+            out.append(None)
+            continue
         C = [int(c) for c in cand[r] if c >= 0]
         f = feedback(p_rows[int(p_row[r])], q_rows[int(q_row[r])], C, int(y_star[r]), W, **kw)
         f["applied"] = 1 if f["severity"] >= w_min else 0

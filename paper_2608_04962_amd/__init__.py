@@ -11,6 +11,7 @@ memory and the current stream.
     commit_path       accepted path's K/V appended to the paged cache, all layers in one launch
     tree_budget       per-response node budget and its tree (Sec. 3.2 Eq. (verification-budget),
                       Eq. (tree-budget)); host-only
+    reflex_feedback   verifier feedback folded into the Reflex memory (Sec. 3.3; Sec. 3.4)
 """
 from __future__ import annotations
 
@@ -21,10 +22,11 @@ from typing import Optional
 import torch
 
 from . import _lib
-from ._lib import AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, SpecRollError, check, lib  # noqa: F401
+from ._lib import (AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, ReflexDesc, SpecRollError,  # noqa: F401
+                   check, lib)
 
 __all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "commit_path", "tree_budget",
-           "prof_begin", "prof_end",
+           "reflex_feedback", "prof_begin", "prof_end",
            "kernel_names", "version", "SpecRollError", "library_path"]
 
 _DT = {torch.float32: _lib.SR_F32, torch.bfloat16: _lib.SR_BF16}
@@ -275,6 +277,55 @@ def commit_path(k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, acc_node
                               _ptr(new_ctx_len), _stream(dev))
     check(st, "sr_commit_path")
     return new_ctx_len
+
+
+REFLEX_DEFAULTS = dict(temperature=1.0, support=48, w_dist=0.15, w_cov=1.25, sev_tv=0.3, sev_out=0.7, w_min=0.03,
+                       eps=1e-6, n_boundary=4)
+REFLEX_RHO = (0.85, 0.90, 0.95)
+
+
+def reflex_feedback(target_logits, p_row, head_logits, q_row, cand, y_star, traj, horizon, W, memory, rho=None,
+                    stats=None, e_out=None, want_e: bool = False, **params):
+    """Fold matured records' verifier feedback into the Reflex memory (in place).
+
+    target_logits [Np,V] bf16|f32, p_row [R] int32, head_logits [Nq,V] f32, q_row [R] int32,
+    cand [R,max_cand] int32 (-1 padded), y_star/traj/horizon [R] int32 (horizon 1-based),
+    W [V,d] bf16|f32, memory [B,H,d] f32. ``rho`` defaults to the paper's (.85, .90, .95), the last value
+    repeated for further horizons. Returns (stats [R,8] f32, e [R,d] f32 or None)."""
+    dev = target_logits.device
+    Np, V = target_logits.shape
+    Nq = head_logits.shape[0]
+    R, MC = cand.shape
+    Bm, Hm, d = memory.shape
+    if target_logits.dtype not in _DT or W.dtype not in _DT:
+        raise TypeError("target_logits and W must be float32 or bfloat16")
+    _need(target_logits, "target_logits", None, (Np, V), dev)
+    _need(head_logits, "head_logits", torch.float32, (Nq, V), dev)
+    for t, n in ((p_row, "p_row"), (q_row, "q_row"), (y_star, "y_star"), (traj, "traj"), (horizon, "horizon")):
+        _need(t, n, torch.int32, (R,), dev)
+    _need(cand, "cand", torch.int32, (R, MC), dev)
+    _need(W, "W", None, (V, d), dev)
+    _need(memory, "memory", torch.float32, (Bm, Hm, d), dev)
+    p = dict(REFLEX_DEFAULTS)
+    p.update(params)
+    rho = list(REFLEX_RHO if rho is None else rho)
+    rho = (rho + [rho[-1]] * 8)[:8]
+    if stats is None:
+        stats = torch.empty((R, 8), dtype=torch.float32, device=dev)
+    _need(stats, "stats", torch.float32, (R, 8), dev)
+    if want_e and e_out is None:
+        e_out = torch.empty((R, d), dtype=torch.float32, device=dev)
+    if e_out is not None:
+        _need(e_out, "e_out", torch.float32, (R, d), dev)
+    desc = ReflexDesc(R, V, d, Bm, Hm, Np, Nq, MC, int(p["support"]), int(p["n_boundary"]),
+                      _DT[target_logits.dtype], _DT[W.dtype], float(p["temperature"]), float(p["w_dist"]),
+                      float(p["w_cov"]), float(p["sev_tv"]), float(p["sev_out"]), float(p["w_min"]), float(p["eps"]),
+                      (C.c_float * 8)(*rho))
+    st = lib().sr_reflex_feedback(C.byref(desc), _ptr(target_logits), _ptr(p_row), _ptr(head_logits), _ptr(q_row),
+                                  _ptr(cand), _ptr(y_star), _ptr(traj), _ptr(horizon), _ptr(W), _ptr(memory),
+                                  _ptr(stats), _ptr(e_out), _stream(dev))
+    check(st, "sr_reflex_feedback")
+    return stats, e_out
 
 
 def prof_begin(kernel_substr: str) -> None:

@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libspecroll.so")
-SOURCES = ["api.hip", "k_heads.hip", "k_attn.hip", "k_accept.hip", "k_engine.hip"]
+SOURCES = ["api.hip", "k_heads.hip", "k_attn.hip", "k_accept.hip", "k_engine.hip", "k_reflex.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -145,7 +145,7 @@ const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
 
 const char* sr_kernel_names(void) {
   return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_tree_attn;"
-         "sr_attn_combine;sr_tree_accept;sr_commit_path";
+         "sr_attn_combine;sr_tree_accept;sr_commit_path;sr_reflex_feedback";
 }
 
 // ------------------------------------------------------------------ proposal
@@ -353,6 +353,38 @@ sr_status sr_commit_path(const sr_commit_desc* d, const int32_t* acc_nodes, cons
   SR_CHECK(new_ctx_len != ctx_len, "new_ctx_len must not overlap ctx_len");
   return launch_commit_path(*d, acc_nodes, out_len, parents, k_tree, v_tree, block_table, ctx_len, k_cache, v_cache,
                             new_ctx_len, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ Reflex feedback
+sr_status sr_reflex_feedback(const sr_reflex_desc* d, const void* target_logits, const int32_t* p_row,
+                             const float* head_logits, const int32_t* q_row, const int32_t* cand,
+                             const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
+                             float* memory, float* stats, float* e_out, void* stream) {
+  SR_CHECK(d != nullptr, "null descriptor");
+  SR_CHECK(d->R >= 1, "R must be >= 1 (got %d)", d->R);
+  SR_CHECK(d->V >= 8 && d->V <= 262144 && d->V % 8 == 0, "V must be a multiple of 8 in [8, 262144] (got %d)", d->V);
+  SR_CHECK(d->d >= 8 && d->d <= 8192 && d->d % 8 == 0, "d must be a multiple of 8 in [8, 8192] (got %d)", d->d);
+  SR_CHECK(d->B >= 1 && d->H >= 1 && d->H <= 8, "need B >= 1 and 1 <= H <= 8");
+  SR_CHECK(d->n_p_rows >= 1 && d->n_q_rows >= 1, "n_p_rows and n_q_rows must be >= 1");
+  SR_CHECK(d->support >= 1 && d->support <= 64 && d->support <= d->V, "support must be in [1, min(64, V)] (got %d)",
+           d->support);
+  SR_CHECK(d->max_cand >= 1 && d->max_cand <= d->support, "max_cand must be in [1, support] (got %d)", d->max_cand);
+  SR_CHECK(d->n_boundary >= 1, "n_boundary must be >= 1");
+  SR_CHECK(dtype_ok(d->p_dtype) && dtype_ok(d->w_dtype), "unknown dtype");
+  SR_CHECK(std::isfinite(d->temperature) && d->temperature > 0.f, "temperature must be finite and > 0");
+  SR_CHECK(std::isfinite(d->eps) && d->eps > 0.f, "eps must be finite and > 0");
+  SR_CHECK(std::isfinite(d->w_dist) && std::isfinite(d->w_cov) && d->w_dist >= 0.f && d->w_cov >= 0.f,
+           "w_dist and w_cov must be finite and >= 0");
+  SR_CHECK(std::isfinite(d->sev_tv) && std::isfinite(d->sev_out) && std::isfinite(d->w_min),
+           "severity coefficients must be finite");
+  for (int h = 0; h < d->H; ++h)
+    SR_CHECK(d->rho[h] >= 0.f && d->rho[h] < 1.f, "rho[%d] must be in [0, 1)", h);
+  SR_CHECK(target_logits && p_row && head_logits && q_row && cand && y_star && traj && horizon && W && memory && stats,
+           "a required pointer is null");
+  SR_CHECK(aligned16(target_logits) && aligned16(head_logits) && aligned16(W),
+           "target_logits, head_logits and W must be 16-byte aligned");
+  return launch_reflex_feedback(*d, target_logits, p_row, head_logits, q_row, cand, y_star, traj, horizon, W, memory,
+                                stats, e_out, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ timing hook

@@ -44,4 +44,10 @@ sr_status launch_commit_path(const sr_commit_desc& d, const int32_t* acc_nodes, 
                              const int32_t* block_table, const int32_t* ctx_len, void* k_cache, void* v_cache,
                              int32_t* new_ctx_len, hipStream_t s);
 
+// ---- Reflex feedback (k_reflex.hip)
+sr_status launch_reflex_feedback(const sr_reflex_desc& d, const void* target_logits, const int32_t* p_row,
+                                 const float* head_logits, const int32_t* q_row, const int32_t* cand,
+                                 const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
+                                 float* memory, float* stats, float* e_out, hipStream_t s);
+
 }  // namespace sr

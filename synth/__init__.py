@@ -28,6 +28,7 @@ _TID = {
     "tlogits": 40, "dnoise": 41, "order": 42, "u_acc": 43, "u_fin": 44,
     "hlogits": 50,
     "ckc": 60, "cvc": 61, "ckt": 62, "cvt": 63, "cacc": 64, "cperm": 65,
+    "rp": 70, "rq": 71, "rcand": 72, "rslot": 73, "rmem": 74, "ry": 75, "rW": 76,
 }
 
 
@@ -426,4 +427,50 @@ def commit_inputs(cfg: Config, seed: int = 0, n_layers: int = 1, with_kv: bool =
             k_cache=as_dtype(kc, cfg.dtype), v_cache=as_dtype(vc, cfg.dtype),
             k_tree=as_dtype(normal(_rng(seed, cfg, "ckt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype),
             v_tree=as_dtype(normal(_rng(seed, cfg, "cvt"), (n_layers, B, T, Hkv, D), 1.0), cfg.dtype))
+    return out
+
+
+def reflex_inputs(cfg: Config, seed: int = 0, R: Optional[int] = None, support: int = 48,
+                  target_std: float = 4.0, boost: float = 8.0, with_W: bool = True) -> dict:
+    """Matured proposal records for the Reflex feedback.
+
+    One record per (trajectory, horizon) slot in a seeded order (the first R of them). Record r's
+    candidate set has K_r = the tree's level size at depth h (capped at ``support``) distinct random
+    tokens. Head logits ~ N(0, target_std) with the candidates raised by ``boost``; target logits
+    ~ N(0, target_std) with a random half of the candidates and as many other random tokens raised by
+    ``boost`` (so part of the target's important mass lies outside the candidates). The realised token is
+    a random raised token. W ~ N(0, 0.02) as in the heads workload; memory ~ N(0, 0.1).
+    """
+    B, H, V, d = cfg.B, cfg.H, cfg.V, cfg.d
+    sizes = level_sizes(cfg.T, cfg.depth) if cfg.T > 1 else [1]
+    slots = [(i, h) for i in range(B) for h in range(1, H + 1)]
+    order = _rng(seed, cfg, "rslot").permutation(len(slots))
+    R = len(slots) if R is None else int(R)
+    recs = [slots[int(j)] for j in order[:R]]
+    K = [max(1, min(support, sizes[min(h, len(sizes)) - 1])) for (_, h) in recs]
+    max_cand = max(K)
+    rng_c, rng_y = _rng(seed, cfg, "rcand"), _rng(seed, cfg, "ry")
+    rng_p, rng_q = _rng(seed, cfg, "rp"), _rng(seed, cfg, "rq")
+    cand = np.full((R, max_cand), -1, dtype=np.int32)
+    p = np.empty((R, V), dtype=np.float32)
+    q = np.empty((R, V), dtype=np.float32)
+    y = np.empty(R, dtype=np.int32)
+    for r in range(R):
+        k = K[r]
+        ids = rng_c.choice(V, 2 * k, replace=False)
+        c, other = ids[:k], ids[k:]
+        cand[r, :k] = c
+        q[r] = normal(rng_q, (V,), target_std)
+        q[r, c] += boost
+        p[r] = normal(rng_p, (V,), target_std)
+        half = c[rng_c.permutation(k)[: max(1, k // 2)]]
+        raised = np.concatenate([half, other])
+        p[r, raised] += boost
+        y[r] = int(raised[int(rng_y.integers(0, raised.shape[0]))])
+    out = dict(cfg=cfg, dtype=cfg.dtype, R=R, support=support, p_logits=as_dtype(p, cfg.dtype), q_logits=q,
+               p_row=np.arange(R, dtype=np.int32), q_row=np.arange(R, dtype=np.int32), cand=cand, y_star=y,
+               traj=np.array([i for i, _ in recs], dtype=np.int32), horizon=np.array([h for _, h in recs], dtype=np.int32),
+               memory=normal(_rng(seed, cfg, "rmem"), (B, H, d), 0.1))
+    if with_W:
+        out["W"] = as_dtype(normal(_rng(seed, cfg, "rW"), (V, d), 0.02), cfg.dtype)
     return out

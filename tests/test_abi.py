@@ -39,6 +39,7 @@ def test_struct_layouts_match_header():
     assert C.sizeof(_lib.AcceptDesc) == 6 * 4
     assert C.sizeof(_lib.CommitDesc) == 10 * 4
     assert C.sizeof(_lib.BudgetDesc) == 4 * 4 + C.sizeof(C.c_void_p)
+    assert C.sizeof(_lib.ReflexDesc) == (12 + 7 + 8) * 4
 
 
 def _call_heads(desc, **ptrs):
@@ -161,3 +162,35 @@ def test_tree_budget_rejections():
                 _lib.BudgetDesc(512, 4, 3, 3, al), _lib.BudgetDesc(512, 1, 129, 3, al),
                 _lib.BudgetDesc(512, 1, 10, 3, None), _lib.BudgetDesc(512, 1, 10, 2, (C.c_int32 * 2)(3, -1))):
         assert lib.sr_tree_budget(C.byref(bad), *args(1, 200)) == _lib.SR_ERR_INVALID
+
+
+def _reflex_desc(**over):
+    d = _lib.ReflexDesc(4, 512, 256, 2, 2, 4, 4, 3, 48, 4, _lib.SR_F32, _lib.SR_F32, 1.0, 0.15, 1.25, 0.3, 0.7,
+                        0.03, 1e-6, (C.c_float * 8)(0.85, 0.9, 0.95, 0.95, 0.95, 0.95, 0.95, 0.95))
+    for k, v in over.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("field,value", [("R", 0), ("V", 12), ("V", 1 << 20), ("d", 12), ("d", 16384), ("H", 9),
+                                         ("support", 0), ("support", 65), ("max_cand", 49), ("max_cand", 0),
+                                         ("n_boundary", 0), ("p_dtype", 4), ("temperature", 0.0), ("eps", 0.0),
+                                         ("w_cov", -1.0), ("n_p_rows", 0)])
+def test_reflex_descriptor_rejected(field, value):
+    fake = C.c_void_p(1 << 20)
+    st = _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc(**{field: value})), *([fake] * 11), None, None)
+    assert st == _lib.SR_ERR_INVALID
+    assert _lib.last_error()
+
+
+def test_reflex_rho_and_pointer_checks():
+    fake = C.c_void_p(1 << 20)
+    d = _reflex_desc()
+    d.rho[1] = 1.0
+    assert _lib.lib().sr_reflex_feedback(C.byref(d), *([fake] * 11), None, None) == _lib.SR_ERR_INVALID
+    args = [fake] * 11
+    args[9] = None                                           # memory
+    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, None, None) == _lib.SR_ERR_INVALID
+    args = [fake] * 11
+    args[8] = C.c_void_p((1 << 20) + 4)                      # misaligned W
+    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, None, None) == _lib.SR_ERR_INVALID
