@@ -483,13 +483,15 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
 
 // ============================================================================ bf16, direct-to-LDS
 // The bf16 path streams K and V tiles from HBM straight into LDS (global_load_lds_dwordx4) through a
-// three-slot ring: while tile i is finished, tiles i+2 and i+3 are in flight. In LDS, 16-byte chunk c of
-// key row k sits at chunk position c ^ (k mod NCH) for K and c ^ ((k / 4) mod NCH) for V, chosen by the
-// source address each lane loads, which keeps the operand reads free of bank conflicts. Once per tile the
-// block transposes V (bf16 -> fp16) into a two-slot V^T ring whose rows hold the keys in the order the
-// MFMA operand wants them, so a V^T fragment is one 16-byte read. Each wave computes the scores of
-// tile i+1 in the same instruction stream as the exponentials of tile i, so its matrix and vector
-// work overlap. One barrier per tile.
+// four-slot ring: while tile i is finished and tile i+1 prepared, tiles i+2 and i+3 are in flight. In LDS,
+// 16-byte chunk c of key row k sits at chunk position c ^ (k mod NCH) for K and c ^ (4 (k mod 4) mod NCH)
+// for V, chosen by the source address each lane loads, which keeps the operand reads free of bank
+// conflicts. Once per tile the block converts the tile's V from bf16 to fp16 in place, and the P V
+// MFMAs read their V^T fragments straight from the row-major tile with the transposing LDS read
+// (ds_read_b64_tr_b16: within 16 lanes, lane i receives element i mod 4 of the 8-byte rows addressed by
+// lanes i/4, 4 + i/4, 8 + i/4 and 12 + i/4, so lanes addressing four keys of four consecutive dims each
+// receive four keys of one dim). Each wave computes the scores of tile i+1 in the same instruction
+// stream as the exponentials of tile i, so its matrix and vector work overlap. One barrier per tile.
 template <int D>
 struct DmaGeom {
   static constexpr int ROWB = D * 2;                   // bytes of one K or V row
@@ -497,18 +499,16 @@ struct DmaGeom {
   static constexpr int KPB = 1024 / ROWB;              // keys per 1 KB DMA block
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
-  static constexpr int VT_ROWB = ATT_KT * 2;           // bytes of one V^T row (64 keys, fp16)
-  static constexpr int VTILE = D * VT_ROWB;
-  static constexpr int TITEMS = (ATT_KT / 4) * (D / 4);  // transpose items of 4 keys x 4 dims
-  static_assert(BLK % ATT_NW == 0 && TITEMS % 64 == 0 && TITEMS <= ATT_NW * 64, "tile split");
+  static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
+  static constexpr int CPL = (CITEMS + 7 * 64 - 1) / (7 * 64);   // chunks per lane with >= 7 converting waves
+  static_assert(BLK % ATT_NW == 0 && CITEMS % 64 == 0, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
 };
 
-// V^T row d: 16-byte slot s holds key groups (4 keys each) g and g + 2 with s = 2*(g/4) + g%2, stored
-// at slot position s ^ vtswz(d); 8 consecutive rows and 8 consecutive even (or odd) rows hit 8 distinct
-// positions, so the fragment reads of 32 rows are conflict-free.
-__device__ __forceinline__ int vtswz(int d) { return (d ^ (d >> 3)) & 7; }
+// chunk-position swizzle of V row k: the eight rows of one transposing read (k mod 4 = 0..3, twice)
+// take four different 64-byte column groups
+template <int NCH> __device__ __forceinline__ int vswz(int k) { return (4 * (k & 3)) & (NCH - 1); }
 
 // Complete this wave's LDS writes and its DMA for the next tile, then meet the block. A wave that
 // issues DMA (one of npd such waves, each with 2*BLK/npd transfers per tile) may leave the transfers
@@ -539,9 +539,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   using G = DmaGeom<D>;
   constexpr int NQF = D / 16;         // Q fragments per lane
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
-  // ring slot: K tile, then raw V tile
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[3][2 * G::TILE];
-  __shared__ __attribute__((aligned(1024))) unsigned char vtr[2][G::VTILE];
+  // ring slot: K tile, then V tile (bf16 as loaded, fp16 once converted)
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * G::TILE];
   __shared__ AttnMeta meta;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
@@ -584,9 +583,9 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
 #pragma unroll
   for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
   float m_run = -INFINITY, l_run = 0.f;
-  // Roles. Without any wave free of query rows, all waves share the DMA and the V transposition. Else
+  // Roles. Without any wave free of query rows, all waves share the DMA and the V conversion. Else
   // the first row-free wave issues all of the DMA (npd = 1), pacing itself on the memory system, and
-  // the other seven waves transpose V.
+  // the other seven waves convert V.
   const int n_act = min(ATT_NW, (R - rg * ATT_ROWS + 31) / 32);
   const int n_prod = ATT_NW - n_act;
   const bool wave_active = wave < n_act && !bad;
@@ -623,7 +622,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     }
     const long long base = tree ? (long long)(kt_b - kc_b) : 0;   // tree rows are addressed from kc_b
     ko = base + off + ((pos ^ (kk & (G::NCH - 1))) * 16);
-    vo = (tree ? (long long)(vt_b - vc_b) : 0) + off + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16);
+    vo = (tree ? (long long)(vt_b - vc_b) : 0) + off + ((pos ^ vswz<G::NCH>(kk)) * 16);
   };
   // every wave issues its BLK/8 blocks of K and of V (all waves have query rows)
   auto issue_dist = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
@@ -655,7 +654,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
         const int kk = blk * G::KPB + ln / G::NCH, pos = ln % G::NCH;
         const long long row = po[kk >> 4] + (kk & 15) * G::ROWB;
         lds_dma16_manual(kc_b + row + ((pos ^ (kk & (G::NCH - 1))) * 16), slot + blk * 1024);
-        lds_dma16_manual(vc_b + row + ((pos ^ ((kk >> 2) & (G::NCH - 1))) * 16), slot + G::TILE + blk * 1024);
+        lds_dma16_manual(vc_b + row + ((pos ^ vswz<G::NCH>(kk)) * 16), slot + G::TILE + blk * 1024);
         __builtin_amdgcn_sched_barrier(0);        // keep each address next to its transfer
       }
     } else {
@@ -671,43 +670,27 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     if (n_prod == 0) issue_dist(i, slot);
     else issue_prod(i, slot);
   };
-  // raw V (bf16, [key][d]) -> V^T (fp16); item = (4-key group kg, 4-dim group dg), two items per lane
-  // at a time with all their reads issued first
-  auto transpose = [&](const unsigned char* rawv, unsigned char* vt) __attribute__((always_inline)) {
+  // V of a tile, bf16 -> fp16 in place: every converting lane takes whole 16-byte chunks (their positions
+  // do not matter), all of its reads issued first
+  auto convert = [&](unsigned char* v) __attribute__((always_inline)) {
     if (tr_rank < 0) return;                    // the DMA wave
     const int stride = n_tr * 64;
     int ln = lane;
     asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
-    for (int it0 = tr_rank * 64 + ln; it0 < G::TITEMS; it0 += 2 * stride) {   // uniform per wave
-      u32x2 r[2][4];
+    u32x4 w[G::CPL];
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int it = it0 + k * stride;
-        if (it < G::TITEMS) {
-          const int kg = it & 15, dg = it >> 4;
-          const int pos = (dg >> 1) ^ (kg & (G::NCH - 1));
+    for (int k = 0; k < G::CPL; ++k) {
+      const int it = tr_rank * 64 + ln + k * stride;
+      if (it < G::CITEMS) w[k] = *(const u32x4*)(v + it * 16);
+    }
 #pragma unroll
-          for (int j = 0; j < 4; ++j) r[k][j] = *(const u32x2*)(rawv + (4 * kg + j) * G::ROWB + pos * 16 + (dg & 1) * 8);
-        }
-      }
+    for (int k = 0; k < G::CPL; ++k) {
+      const int it = tr_rank * 64 + ln + k * stride;
+      if (it < G::CITEMS) {
+        f16x8 h;
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int it = it0 + k * stride;
-        if (it < G::TITEMS) {
-          const int kg = it & 15, dg = it >> 4;
-          const int slot = ((kg >> 2) << 1) | (kg & 1), sub = (kg >> 1) & 1;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int d = 4 * dg + i;
-            f16x4 h;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const uint32_t w = r[k][j][i >> 1];
-              h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
-            }
-            *(f16x4*)(vt + d * G::VT_ROWB + ((slot ^ vtswz(d)) * 16) + sub * 8) = h;
-          }
-        }
+        for (int e = 0; e < 8; ++e) h[e] = (_Float16)bf2f((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
+        *(f16x8*)(v + it * 16) = h;
       }
     }
   };
@@ -728,7 +711,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   };
   // mask, online softmax and O^T += V^T P^T for tile i (scores s); the next tile's scores (K in nks) are
   // computed into sn in the same basic block as this tile's exponentials
-  auto finish = [&](int i, f32x16 (&s)[2], const unsigned char* vt, const unsigned char* nks, f32x16 (&sn)[2]) {
+  auto finish = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2]) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
     const bool full = !tree && t0 + ATT_KT <= key1;
@@ -804,10 +787,22 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     l_run = l_run * alpha + psum;
     constexpr int NPV = 4 * NDT;                  // P V MFMAs per tile
     f16x8 vf[3];
+    // V^T fragment (dims dt*32 + lane%32; keys of k-slot 8*half + j: 16 kq + 8 (j/4) + 4 half + j%4) as two
+    // transposing reads of four keys each: lane s of a 16-lane group addresses key row kb + s/4, dims
+    // d0 + 4 (s mod 4) .. + 3
     auto vread = [&](int j) __attribute__((always_inline)) -> f16x8 {
       const int kt = j / (2 * NDT), kq = (j / NDT) & 1, dt = j % NDT;
-      const int d = dt * 32 + (lane & 31);
-      return *(const f16x8*)(vt + d * G::VT_ROWB + (((4 * kt + 2 * kq + half) ^ vtswz(d)) * 16));
+      const int s16 = lane & 15, d0 = dt * 32 + 16 * ((lane >> 4) & 1);
+      const int col = d0 + 4 * (s16 & 3);             // first of the four dims this lane addresses
+      f16x4 part[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int row = kt * 32 + kq * 16 + 8 * r + 4 * half + (s16 >> 2);
+        const unsigned char* a = vs + row * G::ROWB + (((col >> 3) ^ vswz<G::NCH>(row)) * 16) + (col & 7) * 2;
+        part[r] = __builtin_bit_cast(f16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                (__attribute__((address_space(3))) v4i16*)(a)));
+      }
+      return (f16x8){part[0][0], part[0][1], part[0][2], part[0][3], part[1][0], part[1][1], part[1][2], part[1][3]};
     };
     vf[0] = vread(0);
     vf[1] = vread(1);
@@ -820,16 +815,16 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     }
   };
 
-  // ---- pipeline. step(i): wait for tile i+1, refill the slot tile i used with tile i+3, transpose
-  // V of tile i+1, then finish tile i while computing the scores of tile i+1 (slot of tile i: si).
+  // ---- pipeline. step(i): wait for tile i+1, refill the slot of tile i-1 with tile i+3, convert V of
+  // tile i+1, then finish tile i while computing the scores of tile i+1 (slot of tile i: si).
   f32x16 sa[2], sb[2];
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
-    const int sn_ = si == 2 ? 0 : si + 1;
+    const int sn_ = (si + 1) & 3, sf = (si + 3) & 3;
     attn_sync<D>(npd, dma_wave, i + 2 < n_tiles);
-    if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[si]);
-    if (i + 1 < n_tiles) transpose(ring[sn_] + G::TILE, vtr[(i + 1) & 1]);
+    if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[sf]);
+    if (i + 1 < n_tiles) convert(ring[sn_] + G::TILE);
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
-    if (wave_active) finish(i, s, vtr[i & 1], ring[sn_], sn);
+    if (wave_active) finish(i, s, ring[si] + G::TILE, ring[sn_], sn);
   };
   if (n_tiles > 0) {
     if (dma_wave) {
@@ -838,15 +833,15 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     }
     attn_sync<D>(npd, dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
     if (dma_wave && n_tiles > 2) issue(2, ring[2]);
-    transpose(ring[0] + G::TILE, vtr[0]);
+    convert(ring[0] + G::TILE);
     if (wave_active) qk(ring[0], sa);
     int si = 0;
     for (int i = 0; i < n_tiles; i += 2) {
       step(i, si, sa, sb);
-      si = si == 2 ? 0 : si + 1;
+      si = (si + 1) & 3;
       if (i + 1 < n_tiles) {
         step(i + 1, si, sb, sa);
-        si = si == 2 ? 0 : si + 1;
+        si = (si + 1) & 3;
       }
     }
   }
