@@ -15,9 +15,10 @@ from the paper (SpecRoll, arXiv 2608.04962):
 * ``engine``    -- the concurrency-aware node budget and the tree it allows
                    (Sec. 3.2, Eq. (verification-budget), Eq. (tree-budget)) and
                    the accepted-path cache extraction.
-* ``reflex``    -- verifier feedback directions and the trajectory-local
-                   memory update (Sec. 3.3, Sec. 3.4 Eq. (support) to
-                   Eq. (ema); App. A.1; App. C).
+* ``reflex``    -- verifier feedback directions, the trajectory-local
+                   memory update, delayed-alignment reliability and the gated
+                   head-state correction (Sec. 3.3; Sec. 3.4 Eq. (support) to
+                   Eq. (reflex-correction); App. A.1; App. C).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may use this package. It shares no code with the HIP library and
@@ -29,4 +30,5 @@ from .tree import tree_structure, top_m, sample_ordered_children, tree_build  # 
 from .attention import gather_prefix, tree_attention, tree_attention_node  # noqa: F401
 from .accept import inverse_cdf, tree_accept, tree_accept_one, FALLBACK, BONUS  # noqa: F401
 from .engine import tree_budget, commit_path  # noqa: F401
-from .reflex import feedback, reflex_feedback, ema_update, build_support, top_list  # noqa: F401
+from .reflex import (feedback, reflex_feedback, ema_update, build_support, top_list, sketch,  # noqa: F401
+                     moments_update, reliability, correction)

@@ -113,12 +113,17 @@ def ema_update(m: np.ndarray, e: np.ndarray, rho: float) -> np.ndarray:
 
 def reflex_feedback(p_rows: np.ndarray, p_row: np.ndarray, q_rows: np.ndarray, q_row: np.ndarray,
                     cand: np.ndarray, y_star: np.ndarray, traj: np.ndarray, horizon: np.ndarray, W: np.ndarray,
-                    memory: np.ndarray, rho: Sequence[float], w_min: float = 0.03, rows=None, **kw):
+                    memory: np.ndarray, rho: Sequence[float], w_min: float = 0.03, rows=None, P=None,
+                    rec_sketch=None, align=None, **kw):
     """Batched records with the library's layout: cand [R, max_cand] (-1 padded), horizon 1-based,
     memory [B, H, d]. Records are applied in order; a record whose (trajectory, horizon) slot was already
     used by an earlier record of the batch is skipped (applied = -1). ``rows`` restricts the computation
-    to those records (the others are reported as None). Returns (new memory, list of dicts)."""
+    to those records (the others are reported as None). With ``align`` [B, H, 4] (count, mean, M2 of the
+    alignments, feedback count), an applied record adds one to the feedback count and, given P and the
+    record's proposal-time memory sketch rec_sketch[r] (all zero = none), one alignment observation.
+    Returns (new memory, list of dicts), or (new memory, list, new align) when ``align`` is given."""
     mem = np.array(memory, dtype=np.float64, copy=True)
+    al = None if align is None else np.array(align, dtype=np.float64, copy=True)
     seen = set()
     out = []
     for r in range(cand.shape[0]):
@@ -136,5 +141,68 @@ def reflex_feedback(p_rows: np.ndarray, p_row: np.ndarray, q_rows: np.ndarray, q
         if f["applied"]:
             i, h = slot
             mem[i, h - 1] = ema_update(mem[i, h - 1], f["e"], rho[h - 1])
+            if al is not None:
+                al[i, h - 1, 3] += 1
+                sr_ = None if rec_sketch is None else np.asarray(rec_sketch[r], dtype=np.float64)
+                xi = None if P is None else sketch(f["e"], P)
+                if sr_ is not None and np.any(sr_ != 0.0) and xi is not None:
+                    f["alignment"] = float(sr_ @ xi)
+                    al[i, h - 1, :3] = moments_update(tuple(al[i, h - 1, :3]), f["alignment"])
         out.append(f)
-    return mem, out
+    return (mem, out) if al is None else (mem, out, al)
+
+
+# ----------------------------------------------------------------------------- reliability gate
+# Paper: Sec. 3.4, paragraphs "Reliability from delayed alignment" (Eq. (reliability-score)) and "Gated
+# hidden-state correction" (Eq. (reflex-correction)); App. C, paragraph "Reflex configuration" and
+# Tab. "reflex-hparams": rank-24 normalised random projections, exact online sample moments, minimum
+# feedback counts (1, 2, 4), minimum alignment counts (6, 16, 48), correction intervals (1.0-2.5 %,
+# 0.4-1.0 %, 0.25-0.6 %) of the head state's RMS, z_delta = 0.6.
+#
+# Readings taken here:
+# * sketch(x) = P x / ||P x|| with the caller's projection P [r, d]; undefined (None) when P x = 0.
+# * An alignment observation a = <s, sketch(e)> is taken when a record's feedback is applied, with s the
+#   memory sketch stored when the record was proposed; none when either sketch is undefined.
+# * Moments: count n, mean and M2 by the one-pass update; sample standard deviation sqrt(M2 / (n - 1)).
+# * Rel = mean - z_delta * std / sqrt(n), defined for n >= 2.
+# * The correction is applied iff n_fb >= n_fb_min, n >= n_align_min (and >= 2), Rel > 0 and
+#   RMS(m) > m_floor; then alpha = a_min + (a_max - a_min) * min(Rel, 1) (the interval is spanned by
+#   the reliability score), else alpha = 0.
+# * Horizons past the listed ones reuse the last listed values.
+
+
+def sketch(x: np.ndarray, P: np.ndarray):
+    v = np.asarray(P, dtype=np.float64) @ np.asarray(x, dtype=np.float64)
+    n = float(np.sqrt(np.sum(v * v)))
+    return None if n == 0.0 else v / n
+
+
+def moments_update(stats: Sequence[float], a: float):
+    """One-pass (count, mean, M2) update with observation a."""
+    n, mean, m2 = stats
+    n1 = n + 1
+    d = a - mean
+    mean1 = mean + d / n1
+    return (n1, mean1, m2 + d * (a - mean1))
+
+
+def reliability(stats: Sequence[float], z_delta: float):
+    n, mean, m2 = stats
+    if n < 2:
+        return None
+    return mean - z_delta * np.sqrt(m2 / (n - 1)) / np.sqrt(n)
+
+
+def correction(z: np.ndarray, m: np.ndarray, stats: Sequence[float], n_fb: int, a_min: float, a_max: float,
+               n_fb_min: int, n_align_min: int, z_delta: float = 0.6, eps: float = 1e-6, m_floor: float = 1e-8):
+    """Eq. (reflex-correction) for one (trajectory, horizon): returns (z + dz, alpha, Rel)."""
+    z = np.asarray(z, dtype=np.float64)
+    m = np.asarray(m, dtype=np.float64)
+    rel = reliability(stats, z_delta)
+    ok = (n_fb >= n_fb_min and stats[0] >= max(n_align_min, 2) and rel is not None and rel > 0.0
+          and rms(m) > m_floor)
+    if not ok:
+        return z.copy(), 0.0, rel
+    alpha = a_min + (a_max - a_min) * min(rel, 1.0)
+    u = m / (rms(m) + eps)
+    return z + alpha * rms(z) * u, alpha, rel

@@ -180,3 +180,90 @@ def test_low_severity_record_leaves_memory():
                                        np.array([0]), np.array([0]), np.array([1]), W, mem0, rho=(0.85,))
     assert info[0]["severity"] < 0.03 and info[0]["applied"] == 0
     np.testing.assert_array_equal(mem, mem0)
+
+
+# ----------------------------------------------------------------------------- reliability gate
+def test_moments_match_two_pass_statistics():
+    """The one-pass moments against numpy's two-pass mean and sample variance."""
+    a = np.random.default_rng(3).uniform(-1, 1, 37)
+    st = (0, 0.0, 0.0)
+    for k, x in enumerate(a, 1):
+        st = oracle.moments_update(st, x)
+        assert st[0] == k
+        assert st[1] == pytest.approx(a[:k].mean(), abs=1e-14)
+        if k >= 2:
+            assert st[2] / (k - 1) == pytest.approx(a[:k].var(ddof=1), rel=1e-12)
+
+
+def test_reliability_score_hand_example():
+    # alignments 0.5, 0.7, 0.9: mean 0.7, sample std 0.2, n = 3
+    st = (0, 0.0, 0.0)
+    for x in (0.5, 0.7, 0.9):
+        st = oracle.moments_update(st, x)
+    assert oracle.reliability(st, 0.6) == pytest.approx(0.7 - 0.6 * 0.2 / np.sqrt(3), rel=1e-12)
+    assert oracle.reliability(oracle.moments_update((0, 0.0, 0.0), 0.3), 0.6) is None
+
+
+def test_sketch_is_unit_and_scale_invariant():
+    rng = np.random.default_rng(4)
+    P = rng.standard_normal((24, 40))
+    x = rng.standard_normal(40)
+    s = oracle.sketch(x, P)
+    assert np.linalg.norm(s) == pytest.approx(1.0, rel=1e-14)
+    np.testing.assert_allclose(oracle.sketch(3.5 * x, P), s, rtol=1e-13)
+    np.testing.assert_allclose(oracle.sketch(-x, P), -s, rtol=1e-13)
+    assert oracle.sketch(np.zeros(40), P) is None
+
+
+def _reliable_stats(n=50, mean=0.6, spread=0.1):
+    st = (0, 0.0, 0.0)
+    for k in range(n):
+        st = oracle.moments_update(st, mean + spread * (1 if k % 2 else -1))
+    return st
+
+
+def test_correction_magnitude_direction_and_gates():
+    """Eq. (reflex-correction): dz = alpha RMS(z) m / (RMS(m) + eps), alpha spanned by Rel; every gate
+    condition switches it off."""
+    rng = np.random.default_rng(5)
+    z, m = rng.standard_normal(64), rng.standard_normal(64) * 0.3
+    st = _reliable_stats()
+    rel = oracle.reliability(st, 0.6)
+    zc, alpha, r = oracle.correction(z, m, st, n_fb=5, a_min=0.01, a_max=0.025, n_fb_min=1, n_align_min=6)
+    assert r == pytest.approx(rel) and alpha == pytest.approx(0.01 + 0.015 * rel)
+    dz = zc - z
+    np.testing.assert_allclose(dz / np.linalg.norm(dz), m / np.linalg.norm(m), rtol=1e-12)
+    rms = lambda v: np.sqrt(np.mean(v * v))  # noqa: E731
+    assert rms(dz) == pytest.approx(alpha * rms(z) * rms(m) / (rms(m) + 1e-6), rel=1e-12)
+    # the shadow correction of App. E, Eq. (shadow-correction), has the same form with a fixed ratio
+    zs, a_s, _ = oracle.correction(z, m, st, n_fb=5, a_min=0.005, a_max=0.005, n_fb_min=1, n_align_min=6)
+    np.testing.assert_allclose(zs, z + 0.005 * rms(z) * m / (rms(m) + 1e-6), rtol=1e-13)
+    off = [dict(n_fb=0), dict(n_align_min=51), dict(st=_reliable_stats(mean=-0.2)), dict(m=np.zeros(64))]
+    for o in off:
+        args = dict(z=z, m=m, st=st, n_fb=5, a_min=0.01, a_max=0.025, n_fb_min=1, n_align_min=6)
+        args.update(o)
+        zc, alpha, _ = oracle.correction(args["z"], args["m"], args["st"], args["n_fb"], args["a_min"],
+                                         args["a_max"], args["n_fb_min"], args["n_align_min"])
+        assert alpha == 0.0 and np.array_equal(zc, z)
+
+
+def test_feedback_alignment_observations():
+    rng = np.random.default_rng(6)
+    V, d, B, H = 60, 16, 2, 2
+    W = rng.standard_normal((V, d))
+    P = rng.standard_normal((24, d))
+    p_rows, q_rows = rng.standard_normal((3, V)) * 2, rng.standard_normal((3, V)) * 2
+    cand = np.array([[1, 2, -1], [3, 4, 5], [6, -1, -1]])
+    s_rec = np.zeros((3, 24))
+    s_rec[0] = oracle.sketch(rng.standard_normal(d), P)
+    s_rec[2] = oracle.sketch(rng.standard_normal(d), P)       # record 1 has no stored sketch
+    align0 = np.zeros((B, H, 4))
+    mem, info, al = oracle.reflex_feedback(p_rows, np.arange(3), q_rows, np.arange(3), cand, np.array([7, 8, 9]),
+                                           np.array([0, 1, 0]), np.array([1, 1, 2]), W, np.zeros((B, H, d)),
+                                           rho=(0.85, 0.9), P=P, rec_sketch=s_rec, align=align0)
+    assert all(f["applied"] == 1 for f in info)
+    a0 = float(s_rec[0] @ oracle.sketch(info[0]["e"], P))
+    assert info[0]["alignment"] == pytest.approx(a0, rel=1e-14) and "alignment" not in info[1]
+    np.testing.assert_allclose(al[0, 0], [1, a0, 0.0, 1])
+    np.testing.assert_allclose(al[1, 0], [0, 0.0, 0.0, 1])
+    assert al[0, 1, 0] == 1 and al[0, 1, 3] == 1
