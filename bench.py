@@ -4,10 +4,11 @@ A step is the whole hot path over one batch of synthetic inputs resident in HBM:
   sr_heads_propose (heads + vocabulary projection + draft tree)
   -> sr_tree_verify_attn (tree-masked attention over the paged prefix, one layer)
   -> sr_tree_accept (exact acceptance walk).
-After the timed steps, two calls around the step are timed on their own and reported beside it: the
+After the timed steps, the calls around the step are timed on their own and reported beside it: the
 accepted-path cache commit (sr_commit_path) of the last step's accepted paths for all 28 layers of the
-7B-shaped target, and the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
-horizon) slot on the step's own target-logit rows, head logits and draft trees.
+7B-shaped target, the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
+horizon) slot on the step's own target-logit rows, head logits and draft trees, and the gated head-state
+correction (the sr_reflex_correct kernel of sr_heads_propose_reflex) from the resulting memory.
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
 hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
 
@@ -295,14 +296,35 @@ def reflex_bench(sr, cfg, H, C_, hin, hws, dev):
     ms, n = sr.prof_end()
     st = stats.cpu().numpy()
     assert (st[:, 5] >= 0).all(), "invalid records in the feedback benchmark"
+    # the gated head-state correction from that memory, every gate open (enough aligned evidence)
+    g = torch.Generator(device=dev).manual_seed(0)
+    P = torch.randn((24, d), generator=g, device=dev)
+    P /= P.norm(dim=1, keepdim=True)
+    align = torch.tensor([100.0, 0.9, 99 * 0.0025, 20.0], device=dev).repeat(B, Hh, 1).contiguous()
+    sk = torch.empty((B, Hh, 24), dtype=torch.float32, device=dev)
+    al = torch.empty((B, Hh), dtype=torch.float32, device=dev)
+    run_c = lambda: sr.heads_propose_reflex(  # noqa: E731
+        H["hidden"], None, None, H["A"], H["bias"], H["W"], H["parents"], H["root_token"], H["u_tree"],
+        hin["max_children"], mem, align, P, tokens=tok, child_logit=cl, sketch_out=sk, alpha_out=al, workspace=hws)
+    run_c()
+    torch.cuda.synchronize()
+    sr.prof_begin("sr_reflex_correct")
+    for _ in range(20):
+        run_c()
+    cms, cn = sr.prof_end()
+    assert (al.cpu() > 0).all(), "closed gates in the correction benchmark"
     nS = float(st[:, 4].mean())
     # per record: one target row (bf16), one head row (fp32), the support's rows of W, the memory row in/out
     alg = R * (V * 2 + V * 4 + nS * d * 2 + 2 * d * 4)
     avg = ms / max(n, 1)
     del logits
+    calg = B * Hh * d * (2 + 4 + 2) + 24 * d * 4   # z in and out (bf16), memory row, P
+    cavg = cms / max(cn, 1)
     return {"records": R, "mean_support": nS, "avg_ms": avg, "launches": n, "algorithmic_bytes": alg,
             "GB/s": alg / (avg / 1e3) / 1e9, "frac_hbm_peak": alg / (avg / 1e3) / 1e9 / HBM_PEAK_GBPS,
-            "applied_frac": float((st[:, 5] == 1).mean())}
+            "applied_frac": float((st[:, 5] == 1).mean()),
+            "correct": {"rows": B * Hh, "avg_ms": cavg, "launches": cn, "algorithmic_bytes": calg,
+                        "GB/s": calg / (cavg / 1e3) / 1e9}}
 
 
 def measured_traffic(kernel):

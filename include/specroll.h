@@ -20,8 +20,12 @@
  *                           tree it allows (Sec. 3.2 Eq. (verification-budget),
  *                           Eq. (tree-budget)).
  *   5. sr_reflex_feedback   verifier feedback of matured proposals folded into the
- *                           trajectory-local Reflex memory (Sec. 3.3; Sec. 3.4
- *                           Eq. (support) to Eq. (ema)).
+ *                           trajectory-local Reflex memory and its delayed-alignment
+ *                           statistics (Sec. 3.3; Sec. 3.4 Eq. (support) to Eq. (ema),
+ *                           Eq. (reliability-score)).
+ *      sr_heads_propose_reflex  step 1 with the paper-form gated correction of the
+ *                           head states from that memory (Sec. 3.4
+ *                           Eq. (reflex-correction)).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -372,6 +376,8 @@ typedef struct {
   float w_min;           /* severity gate                                          */
   float eps;             /* RMS stabiliser, > 0                                    */
   float rho[8];          /* per-horizon decay in [0, 1), entries 0..H-1 used       */
+  int32_t rank;          /* rows of the sketch projection P, 0..64 (0 = no alignment
+                            observations)                                          */
 } sr_reflex_desc;
 
 /*
@@ -392,6 +398,14 @@ typedef struct {
  *                                      -2 (invalid record); the other entries are NaN for -1 and -2
  * e_out         [R,d]         fp32     OUT (optional, NULL = not written) the feedback vector e
  *                                      (NaN rows for skipped and invalid records)
+ * P             [rank,d]      fp32     sketch projection (NULL when rank == 0), 16-byte aligned
+ * rec_sketch    [R,rank]      fp32     unit memory sketch stored when record r was proposed (as
+ *                                      sr_heads_propose_reflex writes it); all zero = none
+ * align         [B,H,4]       fp32     IN/OUT (optional, NULL = not kept) per (i, h): count, mean and M2
+ *                                      of the alignments, and the count of applied feedback records.
+ *                                      An applied record adds 1 to the last; with rank > 0 and a stored
+ *                                      sketch s it adds the observation a = <s, P e / |P e|> to the
+ *                                      moments by the one-pass update (no observation when P e = 0)
  * Invalid record: a row index, trajectory, horizon, y* or candidate id out of
  * range, duplicate candidates, a candidate after a -1, or no candidate.
  * Records are independent blocks; memory rows of distinct (i, h) are written by
@@ -401,7 +415,56 @@ typedef struct {
 sr_status sr_reflex_feedback(const sr_reflex_desc* desc, const void* target_logits, const int32_t* p_row,
                              const float* head_logits, const int32_t* q_row, const int32_t* cand,
                              const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
-                             float* memory, float* stats, float* e_out, void* stream);
+                             float* memory, float* stats, float* e_out, const float* P, const float* rec_sketch,
+                             float* align, void* stream);
+
+/*
+ * Gated head-state correction (Sec. 3.4 "Reliability from delayed alignment",
+ * Eq. (reliability-score); "Gated hidden-state correction", Eq. (reflex-correction);
+ * App. C "Reflex configuration", Tab. "reflex-hparams"). For trajectory b and head
+ * h (horizon h+1, 0-based h here) with memory m = memory[b][h], alignment moments
+ * (n, mean, M2) and feedback count n_fb = align[b][h]:
+ *   Rel   = mean - z_delta * sqrt(M2 / (n - 1)) / sqrt(n)               (n >= 2)
+ *   gate  = n_fb >= n_fb_min[h] and n >= max(n_align_min[h], 2) and Rel > 0
+ *           and RMS(m) > m_floor
+ *   alpha = gate ? alpha_min[h] + (alpha_max[h] - alpha_min[h]) * min(Rel, 1) : 0
+ *   z~    = z + alpha * RMS(z) * m / (RMS(m) + eps), rounded to the head dtype
+ * and the memory sketch P m / |P m| (zero when P m = 0) is written for the caller
+ * to store with the records proposed now. The paper's settings: z_delta 0.6,
+ * n_fb_min (1, 2, 4), n_align_min (6, 16, 48), intervals (1.0-2.5 %, 0.4-1.0 %,
+ * 0.25-0.6 %), the last entry reused for further heads.
+ */
+typedef struct {
+  int32_t rank;          /* rows of P, 0..64 (0 = no sketches)                     */
+  float z_delta;         /* >= 0                                                   */
+  float eps;             /* > 0                                                    */
+  float m_floor;         /* >= 0: memory with RMS <= m_floor is negligible          */
+  float alpha_min[8];    /* per head, 0 <= alpha_min <= alpha_max                  */
+  float alpha_max[8];
+  int32_t n_fb_min[8];   /* per head, >= 0                                         */
+  int32_t n_align_min[8];
+} sr_reflex_gate_desc;
+
+/*
+ * Step 1 (sr_heads_propose) with the gated correction applied to the head states
+ * between the head GEMM and the vocabulary projection. Arguments as
+ * sr_heads_propose (H <= 8; the workspace size is sr_heads_propose_workspace's),
+ * plus:
+ * memory      [B,H,d]     fp32  Reflex memory
+ * align       [B,H,4]     fp32  alignment moments and feedback counts (sr_reflex_feedback's)
+ * P           [rank,d]    fp32  sketch projection (NULL when rank == 0), 16-byte aligned
+ * sketch_out  [B,H,rank]  fp32  OUT (optional) unit memory sketch of every (b, h)
+ * alpha_out   [B,H]       fp32  OUT (optional) the applied ratio alpha (0 = no correction)
+ * z then holds z~ when requested.
+ */
+sr_status sr_heads_propose_reflex(const sr_heads_desc* desc, const sr_reflex_gate_desc* gate,
+                                  const void* hidden, const float* corr, const uint8_t* corr_active,
+                                  const void* A, const void* bias, const void* W,
+                                  const int32_t* parents, const int32_t* root_token, const float* u_tree,
+                                  const float* memory, const float* align, const float* P,
+                                  float* logits, void* z, int32_t* tokens, float* child_logit,
+                                  float* sketch_out, float* alpha_out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* ========================================================================== *
  * Kernel timing hook

@@ -11,7 +11,10 @@ memory and the current stream.
     commit_path       accepted path's K/V appended to the paged cache, all layers in one launch
     tree_budget       per-response node budget and its tree (Sec. 3.2 Eq. (verification-budget),
                       Eq. (tree-budget)); host-only
-    reflex_feedback   verifier feedback folded into the Reflex memory (Sec. 3.3; Sec. 3.4)
+    reflex_feedback   verifier feedback folded into the Reflex memory and its alignment statistics
+                      (Sec. 3.3; Sec. 3.4)
+    heads_propose_reflex  heads_propose with the gated Reflex correction of the head states
+                      (Sec. 3.4 Eq. (reflex-correction))
 """
 from __future__ import annotations
 
@@ -22,11 +25,11 @@ from typing import Optional
 import torch
 
 from . import _lib
-from ._lib import (AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, ReflexDesc, SpecRollError,  # noqa: F401
-                   check, lib)
+from ._lib import (AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, ReflexDesc, ReflexGateDesc,  # noqa: F401
+                   SpecRollError, check, lib)
 
 __all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "commit_path", "tree_budget",
-           "reflex_feedback", "prof_begin", "prof_end",
+           "reflex_feedback", "heads_propose_reflex", "prof_begin", "prof_end",
            "kernel_names", "version", "SpecRollError", "library_path"]
 
 _DT = {torch.float32: _lib.SR_F32, torch.bfloat16: _lib.SR_BF16}
@@ -285,13 +288,15 @@ REFLEX_RHO = (0.85, 0.90, 0.95)
 
 
 def reflex_feedback(target_logits, p_row, head_logits, q_row, cand, y_star, traj, horizon, W, memory, rho=None,
-                    stats=None, e_out=None, want_e: bool = False, **params):
+                    stats=None, e_out=None, want_e: bool = False, P=None, rec_sketch=None, align=None, **params):
     """Fold matured records' verifier feedback into the Reflex memory (in place).
 
     target_logits [Np,V] bf16|f32, p_row [R] int32, head_logits [Nq,V] f32, q_row [R] int32,
     cand [R,max_cand] int32 (-1 padded), y_star/traj/horizon [R] int32 (horizon 1-based),
     W [V,d] bf16|f32, memory [B,H,d] f32. ``rho`` defaults to the paper's (.85, .90, .95), the last value
-    repeated for further horizons. Returns (stats [R,8] f32, e [R,d] f32 or None)."""
+    repeated for further horizons. With ``align`` [B,H,4] f32 (in place) the applied records update the
+    alignment moments, given the sketch projection P [r,d] f32 and the records' stored memory sketches
+    rec_sketch [R,r] f32. Returns (stats [R,8] f32, e [R,d] f32 or None)."""
     dev = target_logits.device
     Np, V = target_logits.shape
     Nq = head_logits.shape[0]
@@ -317,15 +322,97 @@ def reflex_feedback(target_logits, p_row, head_logits, q_row, cand, y_star, traj
         e_out = torch.empty((R, d), dtype=torch.float32, device=dev)
     if e_out is not None:
         _need(e_out, "e_out", torch.float32, (R, d), dev)
+    rank = 0
+    if P is not None:
+        rank = P.shape[0]
+        _need(P, "P", torch.float32, (rank, d), dev)
+        if rec_sketch is not None:
+            _need(rec_sketch, "rec_sketch", torch.float32, (R, rank), dev)
+    if align is not None:
+        _need(align, "align", torch.float32, (Bm, Hm, 4), dev)
     desc = ReflexDesc(R, V, d, Bm, Hm, Np, Nq, MC, int(p["support"]), int(p["n_boundary"]),
                       _DT[target_logits.dtype], _DT[W.dtype], float(p["temperature"]), float(p["w_dist"]),
                       float(p["w_cov"]), float(p["sev_tv"]), float(p["sev_out"]), float(p["w_min"]), float(p["eps"]),
-                      (C.c_float * 8)(*rho))
+                      (C.c_float * 8)(*rho), rank)
     st = lib().sr_reflex_feedback(C.byref(desc), _ptr(target_logits), _ptr(p_row), _ptr(head_logits), _ptr(q_row),
                                   _ptr(cand), _ptr(y_star), _ptr(traj), _ptr(horizon), _ptr(W), _ptr(memory),
-                                  _ptr(stats), _ptr(e_out), _stream(dev))
+                                  _ptr(stats), _ptr(e_out), _ptr(P), _ptr(rec_sketch), _ptr(align), _stream(dev))
     check(st, "sr_reflex_feedback")
     return stats, e_out
+
+
+GATE_DEFAULTS = dict(z_delta=0.6, eps=1e-6, m_floor=1e-8, alpha_min=(0.010, 0.004, 0.0025),
+                     alpha_max=(0.025, 0.010, 0.006), n_fb_min=(1, 2, 4), n_align_min=(6, 16, 48))
+
+
+def _per_head(v, H):
+    v = list(v)
+    return (v + [v[-1]] * 8)[:8]
+
+
+def reflex_gate_desc(rank: int = 0, **params) -> ReflexGateDesc:
+    """Gate parameters (the paper's by default); per-head lists are extended with their last value."""
+    p = dict(GATE_DEFAULTS)
+    p.update(params)
+    return ReflexGateDesc(int(rank), float(p["z_delta"]), float(p["eps"]), float(p["m_floor"]),
+                          (C.c_float * 8)(*_per_head(p["alpha_min"], 8)), (C.c_float * 8)(*_per_head(p["alpha_max"], 8)),
+                          (C.c_int32 * 8)(*_per_head(p["n_fb_min"], 8)), (C.c_int32 * 8)(*_per_head(p["n_align_min"], 8)))
+
+
+def heads_propose_reflex(hidden, corr, corr_active, A, bias, W, parents, root_token, u_tree, max_children: int,
+                         memory, align, P=None, clip_norm: float = 1.0, ln_eps: float = 1e-5,
+                         logits: Optional[torch.Tensor] = None, z: Optional[torch.Tensor] = None,
+                         tokens: Optional[torch.Tensor] = None, child_logit: Optional[torch.Tensor] = None,
+                         sketch_out: Optional[torch.Tensor] = None, alpha_out: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None, **gate):
+    """heads_propose with the gated Reflex correction of the head states. memory [B,H,d] f32,
+    align [B,H,4] f32, P [r,d] f32 or None; sketch_out [B,H,r] and alpha_out [B,H] are optional outputs.
+    Returns (tokens, child_logit)."""
+    dev = hidden.device
+    B, d = hidden.shape
+    H = A.shape[0]
+    V = W.shape[0]
+    T = parents.shape[1]
+    dt = hidden.dtype
+    if dt not in _DT:
+        raise TypeError("hidden must be float32 or bfloat16")
+    _need(hidden, "hidden", None, (B, d), dev)
+    _need(A, "A", dt, (H, d, d), dev)
+    _need(bias, "bias", dt, (H, d), dev)
+    _need(W, "W", dt, (V, d), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    _need(root_token, "root_token", torch.int32, (B,), dev)
+    _need(u_tree, "u_tree", torch.float32, (B, T), dev)
+    _need(memory, "memory", torch.float32, (B, H, d), dev)
+    _need(align, "align", torch.float32, (B, H, 4), dev)
+    if corr is not None:
+        _need(corr, "corr", torch.float32, (B, d), dev)
+    if corr_active is not None:
+        _need(corr_active, "corr_active", torch.uint8, (B,), dev)
+    rank = 0
+    if P is not None:
+        rank = P.shape[0]
+        _need(P, "P", torch.float32, (rank, d), dev)
+    if logits is not None:
+        _need(logits, "logits", torch.float32, (B, H, V), dev)
+    if z is not None:
+        _need(z, "z", dt, (B, H, d), dev)
+    if sketch_out is not None:
+        _need(sketch_out, "sketch_out", torch.float32, (B, H, rank), dev)
+    if alpha_out is not None:
+        _need(alpha_out, "alpha_out", torch.float32, (B, H), dev)
+    tokens = torch.empty((B, T), dtype=torch.int32, device=dev) if tokens is None else tokens
+    child_logit = torch.empty((B, T), dtype=torch.float32, device=dev) if child_logit is None else child_logit
+    desc = HeadsDesc(B, d, H, V, T, int(max_children), _DT[dt], float(clip_norm), float(ln_eps))
+    gdesc = reflex_gate_desc(rank, **gate)
+    ws, wsb = _workspace(int(lib().sr_heads_propose_workspace(C.byref(desc))), dev, workspace)
+    st = lib().sr_heads_propose_reflex(C.byref(desc), C.byref(gdesc), _ptr(hidden), _ptr(corr), _ptr(corr_active),
+                                       _ptr(A), _ptr(bias), _ptr(W), _ptr(parents), _ptr(root_token), _ptr(u_tree),
+                                       _ptr(memory), _ptr(align), _ptr(P), _ptr(logits), _ptr(z), _ptr(tokens),
+                                       _ptr(child_logit), _ptr(sketch_out), _ptr(alpha_out), _ptr(ws), wsb,
+                                       _stream(dev))
+    check(st, "sr_heads_propose_reflex")
+    return tokens, child_logit
 
 
 def prof_begin(kernel_substr: str) -> None:

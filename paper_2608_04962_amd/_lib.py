@@ -51,7 +51,14 @@ class ReflexDesc(C.Structure):
                 ("n_p_rows", C.c_int32), ("n_q_rows", C.c_int32), ("max_cand", C.c_int32), ("support", C.c_int32),
                 ("n_boundary", C.c_int32), ("p_dtype", C.c_int32), ("w_dtype", C.c_int32),
                 ("temperature", C.c_float), ("w_dist", C.c_float), ("w_cov", C.c_float), ("sev_tv", C.c_float),
-                ("sev_out", C.c_float), ("w_min", C.c_float), ("eps", C.c_float), ("rho", C.c_float * 8)]
+                ("sev_out", C.c_float), ("w_min", C.c_float), ("eps", C.c_float), ("rho", C.c_float * 8),
+                ("rank", C.c_int32)]
+
+
+class ReflexGateDesc(C.Structure):
+    _fields_ = [("rank", C.c_int32), ("z_delta", C.c_float), ("eps", C.c_float), ("m_floor", C.c_float),
+                ("alpha_min", C.c_float * 8), ("alpha_max", C.c_float * 8), ("n_fb_min", C.c_int32 * 8),
+                ("n_align_min", C.c_int32 * 8)]
 
 
 # name -> (restype, argtypes)
@@ -72,7 +79,10 @@ SIGNATURES = {
                                  C.c_size_t, _p]),
     "sr_tree_budget": (C.c_int, [C.POINTER(BudgetDesc), C.c_int32, _i32p, _i32p, _i32p, C.c_int32, _i32p]),
     "sr_commit_path": (C.c_int, [C.POINTER(CommitDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]),
-    "sr_reflex_feedback": (C.c_int, [C.POINTER(ReflexDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]),
+    "sr_reflex_feedback": (C.c_int, [C.POINTER(ReflexDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+                                     _p, _p]),
+    "sr_heads_propose_reflex": (C.c_int, [C.POINTER(HeadsDesc), C.POINTER(ReflexGateDesc), _p, _p, _p, _p, _p, _p,
+                                          _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, C.c_size_t, _p]),
     "sr_prof_begin": (C.c_int, [C.c_char_p]),
     "sr_prof_end": (C.c_int, [C.POINTER(C.c_double), _i32p]),
 }

@@ -145,7 +145,7 @@ const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
 
 const char* sr_kernel_names(void) {
   return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_tree_attn;"
-         "sr_attn_combine;sr_tree_accept;sr_commit_path;sr_reflex_feedback";
+         "sr_attn_combine;sr_tree_accept;sr_commit_path;sr_reflex_feedback;sr_reflex_correct";
 }
 
 // ------------------------------------------------------------------ proposal
@@ -176,6 +176,52 @@ sr_status sr_heads_propose(const sr_heads_desc* d, const void* hidden, const flo
   hipStream_t s = (hipStream_t)stream;
   float* gmax = (float*)(ws + L.gmax);
   st = launch_heads(*d, hidden, corr, corr_active, A, bias, W, x, n, zz, lg, gmax, s);
+  if (st != SR_OK) return st;
+  return launch_tree_build(*d, lg, gmax, (int32_t*)(ws + L.need), parents, root_token, u_tree, tokens, child_logit,
+                           (int32_t*)(ws + L.top_id), (float*)(ws + L.top_val), s);
+}
+
+sr_status sr_heads_propose_reflex(const sr_heads_desc* d, const sr_reflex_gate_desc* g, const void* hidden,
+                                  const float* corr, const uint8_t* corr_active, const void* A, const void* bias,
+                                  const void* W, const int32_t* parents, const int32_t* root_token,
+                                  const float* u_tree, const float* memory, const float* align, const float* P,
+                                  float* logits, void* z, int32_t* tokens, float* child_logit, float* sketch_out,
+                                  float* alpha_out, void* workspace, size_t workspace_bytes, void* stream) {
+  sr_status st = check_heads_desc(d, false);
+  if (st != SR_OK) return st;
+  SR_CHECK(g != nullptr, "null gate descriptor");
+  SR_CHECK(d->H <= 8, "H must be <= 8 with the gated correction (got %d)", d->H);
+  SR_CHECK(d->d <= 8192, "d must be <= 8192 with the gated correction (got %d)", d->d);
+  SR_CHECK(g->rank >= 0 && g->rank <= 64, "rank must be in [0, 64] (got %d)", g->rank);
+  SR_CHECK(std::isfinite(g->z_delta) && g->z_delta >= 0.f, "z_delta must be finite and >= 0");
+  SR_CHECK(std::isfinite(g->eps) && g->eps > 0.f, "eps must be finite and > 0");
+  SR_CHECK(std::isfinite(g->m_floor) && g->m_floor >= 0.f, "m_floor must be finite and >= 0");
+  for (int h = 0; h < d->H; ++h) {
+    SR_CHECK(std::isfinite(g->alpha_min[h]) && std::isfinite(g->alpha_max[h]) && g->alpha_min[h] >= 0.f &&
+                 g->alpha_min[h] <= g->alpha_max[h],
+             "need 0 <= alpha_min <= alpha_max (head %d)", h);
+    SR_CHECK(g->n_fb_min[h] >= 0 && g->n_align_min[h] >= 0, "minimum counts must be >= 0 (head %d)", h);
+  }
+  SR_CHECK(hidden && A && bias && W && parents && root_token && u_tree && tokens && child_logit && memory && align,
+           "a required pointer is null");
+  SR_CHECK(g->rank == 0 || P != nullptr, "P is null with rank > 0");
+  SR_CHECK(P == nullptr || aligned16(P), "P must be 16-byte aligned");
+  SR_CHECK(aligned16(hidden) && aligned16(A) && aligned16(W) && aligned16(bias), "hidden/A/bias/W must be 16-byte aligned");
+  SR_CHECK(z == nullptr || aligned16(z), "z must be 16-byte aligned");
+  SR_CHECK(logits == nullptr || aligned16(logits), "logits must be 16-byte aligned");
+  const HeadsLayout L = heads_layout(*d, z == nullptr, logits == nullptr);
+  st = check_ws(workspace, workspace_bytes, L.total);
+  if (st != SR_OK) return st;
+  char* ws = (char*)workspace;
+  void* zz = z ? z : (void*)(ws + L.z);
+  float* lg = logits ? logits : (float*)(ws + L.logits);
+  float* gmax = (float*)(ws + L.gmax);
+  hipStream_t s = (hipStream_t)stream;
+  st = launch_heads_z(*d, hidden, corr, corr_active, A, bias, (float*)(ws + L.x), ws + L.n, zz, s);
+  if (st != SR_OK) return st;
+  st = launch_reflex_correct(*d, *g, zz, memory, align, P, sketch_out, alpha_out, s);
+  if (st != SR_OK) return st;
+  st = launch_vocab(*d, zz, W, lg, gmax, s);
   if (st != SR_OK) return st;
   return launch_tree_build(*d, lg, gmax, (int32_t*)(ws + L.need), parents, root_token, u_tree, tokens, child_logit,
                            (int32_t*)(ws + L.top_id), (float*)(ws + L.top_val), s);
@@ -359,7 +405,8 @@ sr_status sr_commit_path(const sr_commit_desc* d, const int32_t* acc_nodes, cons
 sr_status sr_reflex_feedback(const sr_reflex_desc* d, const void* target_logits, const int32_t* p_row,
                              const float* head_logits, const int32_t* q_row, const int32_t* cand,
                              const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
-                             float* memory, float* stats, float* e_out, void* stream) {
+                             float* memory, float* stats, float* e_out, const float* P, const float* rec_sketch,
+                             float* align, void* stream) {
   SR_CHECK(d != nullptr, "null descriptor");
   SR_CHECK(d->R >= 1, "R must be >= 1 (got %d)", d->R);
   SR_CHECK(d->V >= 8 && d->V <= 262144 && d->V % 8 == 0, "V must be a multiple of 8 in [8, 262144] (got %d)", d->V);
@@ -379,12 +426,16 @@ sr_status sr_reflex_feedback(const sr_reflex_desc* d, const void* target_logits,
            "severity coefficients must be finite");
   for (int h = 0; h < d->H; ++h)
     SR_CHECK(d->rho[h] >= 0.f && d->rho[h] < 1.f, "rho[%d] must be in [0, 1)", h);
+  SR_CHECK(d->rank >= 0 && d->rank <= 64, "rank must be in [0, 64] (got %d)", d->rank);
+  SR_CHECK(d->rank == 0 || align == nullptr || (P != nullptr && rec_sketch != nullptr),
+           "P and rec_sketch are required for alignment observations with rank > 0");
+  SR_CHECK(P == nullptr || aligned16(P), "P must be 16-byte aligned");
   SR_CHECK(target_logits && p_row && head_logits && q_row && cand && y_star && traj && horizon && W && memory && stats,
            "a required pointer is null");
   SR_CHECK(aligned16(target_logits) && aligned16(head_logits) && aligned16(W),
            "target_logits, head_logits and W must be 16-byte aligned");
   return launch_reflex_feedback(*d, target_logits, p_row, head_logits, q_row, cand, y_star, traj, horizon, W, memory,
-                                stats, e_out, (hipStream_t)stream);
+                                stats, e_out, P, rec_sketch, align, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ timing hook

@@ -609,57 +609,69 @@ __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict_
 
 // ============================================================================ launchers
 template <typename T>
-static sr_status launch_heads_t(const sr_heads_desc& d, const void* hidden, const float* corr,
-                                const uint8_t* active, const void* A, const void* bias, const void* W,
-                                float* x, void* n, void* z, float* logits, float* gmax, hipStream_t s) {
+static sr_status launch_heads_z_t(const sr_heads_desc& d, const void* hidden, const float* corr,
+                                  const uint8_t* active, const void* A, const void* bias, float* x, void* n, void* z,
+                                  hipStream_t s) {
   SR_LAUNCH("sr_clip_ln", (k_clip_ln<T>), dim3(d.B), dim3(256), 0, s, (const T*)hidden, corr, active, d.d,
             d.clip_norm, d.ln_eps, x, (T*)n);
   if constexpr (sizeof(T) == 2) {
-    {
-      constexpr int BM = 128, BN = 64, BK = 32;
-      EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
-      const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
-      dim3 grid(((tn + 7) / 8) * 8 * tm);
-      SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
-                (const T*)A, d.B, d.H * d.d, d.d, tm, tn, epi);
-    }
-    {
-      constexpr int BM = 256, BN = 256, BK = 32;
-      const int M = d.B * d.H;
-      EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
-      const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
-      dim3 grid(((tn + 7) / 8) * 8 * tm);
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), grid, dim3(512), 0, s,
-                (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
-    }
+    constexpr int BM = 128, BN = 64, BK = 32;
+    EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
+    const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
+    dim3 grid(((tn + 7) / 8) * 8 * tm);
+    SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+              (const T*)A, d.B, d.H * d.d, d.d, tm, tn, epi);
   } else {
-    {
-      constexpr int BM = 64, BN = 128, BK = 32;
-      EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
-      dim3 grid((d.H * d.d + BN - 1) / BN, (d.B + BM - 1) / BM);
-      SR_LAUNCH("sr_head_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
-                (const T*)A, d.B, d.H * d.d, d.d, epi);
-    }
-    {
-      constexpr int BM = 128, BN = 128, BK = 32;
-      EpiLogits epi{logits, d.V};
-      const int M = d.B * d.H;
-      dim3 grid((d.V + BN - 1) / BN, (M + BM - 1) / BM);
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiLogits>), grid, dim3(256), 0, s, (const T*)z,
-                (const T*)W, M, d.V, d.d, epi);
-      const int ng = (d.V + 63) / 64;
-      SR_LAUNCH("sr_group_max", k_group_max, dim3((ng + 3) / 4, M), dim3(256), 0, s, logits, d.V, ng, gmax);
-    }
+    constexpr int BM = 64, BN = 128, BK = 32;
+    EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
+    dim3 grid((d.H * d.d + BN - 1) / BN, (d.B + BM - 1) / BM);
+    SR_LAUNCH("sr_head_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+              (const T*)A, d.B, d.H * d.d, d.d, epi);
   }
   return SR_OK;
+}
+
+template <typename T>
+static sr_status launch_vocab_t(const sr_heads_desc& d, const void* z, const void* W, float* logits, float* gmax,
+                                hipStream_t s) {
+  const int M = d.B * d.H;
+  if constexpr (sizeof(T) == 2) {
+    constexpr int BM = 256, BN = 256, BK = 32;
+    EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
+    const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
+    dim3 grid(((tn + 7) / 8) * 8 * tm);
+    SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), grid, dim3(512), 0, s,
+              (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+  } else {
+    constexpr int BM = 128, BN = 128, BK = 32;
+    EpiLogits epi{logits, d.V};
+    dim3 grid((d.V + BN - 1) / BN, (M + BM - 1) / BM);
+    SR_LAUNCH("sr_vocab_gemm", (k_gemm<T, BM, BN, BK, 2, 2, EpiLogits>), grid, dim3(256), 0, s, (const T*)z,
+              (const T*)W, M, d.V, d.d, epi);
+    const int ng = (d.V + 63) / 64;
+    SR_LAUNCH("sr_group_max", k_group_max, dim3((ng + 3) / 4, M), dim3(256), 0, s, logits, d.V, ng, gmax);
+  }
+  return SR_OK;
+}
+
+sr_status launch_heads_z(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
+                         const void* A, const void* bias, float* x, void* n, void* z, hipStream_t s) {
+  if (d.dtype == SR_BF16) return launch_heads_z_t<bf16_t>(d, hidden, corr, active, A, bias, x, n, z, s);
+  return launch_heads_z_t<float>(d, hidden, corr, active, A, bias, x, n, z, s);
+}
+
+sr_status launch_vocab(const sr_heads_desc& d, const void* z, const void* W, float* logits, float* gmax,
+                       hipStream_t s) {
+  if (d.dtype == SR_BF16) return launch_vocab_t<bf16_t>(d, z, W, logits, gmax, s);
+  return launch_vocab_t<float>(d, z, W, logits, gmax, s);
 }
 
 sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
                        const void* A, const void* bias, const void* W, float* x, void* n, void* z,
                        float* logits, float* gmax, hipStream_t s) {
-  if (d.dtype == SR_BF16)
-    return launch_heads_t<bf16_t>(d, hidden, corr, active, A, bias, W, x, n, z, logits, gmax, s);
-  return launch_heads_t<float>(d, hidden, corr, active, A, bias, W, x, n, z, logits, gmax, s);
+  sr_status st = launch_heads_z(d, hidden, corr, active, A, bias, x, n, z, s);
+  if (st != SR_OK) return st;
+  return launch_vocab(d, z, W, logits, gmax, s);
 }
 
 sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax, int32_t* need_full,

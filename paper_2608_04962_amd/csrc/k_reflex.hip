@@ -68,6 +68,7 @@ struct RfSmem {
   int S[RF_MAXS];
   float ca[RF_MAXS], cb[RF_MAXS];   // coefficients of the support rows in r_dist and r_cov
   double red[RF_NW][2];
+  double xr[RF_NW][RF_MAXS];      // per-wave partial sketch projections
   float Mrow;
   double Zrow;
   int nS, bad;
@@ -235,7 +236,8 @@ __global__ __launch_bounds__(RF_NT) void k_reflex_feedback(
     const TP* __restrict__ plog, const int32_t* __restrict__ p_row, const float* __restrict__ qlog,
     const int32_t* __restrict__ q_row, const int32_t* __restrict__ cand, const int32_t* __restrict__ y_star,
     const int32_t* __restrict__ traj, const int32_t* __restrict__ horizon, const TW* __restrict__ W,
-    float* __restrict__ memory, float* __restrict__ stats, float* __restrict__ e_out, sr_reflex_desc d) {
+    float* __restrict__ memory, float* __restrict__ stats, float* __restrict__ e_out, const float* __restrict__ P,
+    const float* __restrict__ rec_sketch, float* __restrict__ align, sr_reflex_desc d) {
   __shared__ RfSmem sm;
   const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int V = d.V, KS = d.support, MC = d.max_cand;
@@ -455,6 +457,66 @@ __global__ __launch_bounds__(RF_NT) void k_reflex_feedback(
       }
     }
   }
+  // ---- delayed alignment: the applied record's feedback sketch against the memory sketch stored at
+  // proposal time (Sec. 3.4 "Reliability from delayed alignment"), one-pass moments per slot
+  if (align != nullptr && apply) {
+    float* al = align + ((size_t)ti * d.H + (hz - 1)) * 4;
+    const int rk = d.rank;
+    if (rk > 0 && P != nullptr && rec_sketch != nullptr) {
+      // sixteen rows at a time: their loads first, then one wave reduction per row
+      constexpr int JB = 16;
+      for (int j0 = 0; j0 < rk; j0 += JB) {
+        float part[JB];
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int j = j0 + jj;
+          part[jj] = 0.f;
+          if (j < rk) {
+            const float* pj = P + (size_t)j * dcols;
+#pragma unroll
+            for (int gi = 0; gi < RF_CG; ++gi) {
+              const int c0 = (tid + gi * RF_NT) * 8;
+              if (c0 < dcols) {
+                float pv[8];
+                RfRow<float>::load8(pj + c0, pv);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) part[jj] = fmaf(pv[e], ke * g[gi][e], part[jj]);
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int j = j0 + jj;
+          if (j < rk) {
+            const double v = wave_sum_f64((double)part[jj]);
+            if (lane == 0) sm.xr[wave][j] = v;
+          }
+        }
+      }
+      __syncthreads();
+      if (tid == 0) {
+        double nx = 0.0, ns = 0.0, dot = 0.0;
+        const float* sr = rec_sketch + (size_t)r * rk;
+        for (int j = 0; j < rk; ++j) {
+          double x = 0.0;
+          for (int w = 0; w < RF_NW; ++w) x += sm.xr[w][j];
+          nx += x * x;
+          ns += (double)sr[j] * sr[j];
+          dot += (double)sr[j] * x;
+        }
+        if (nx > 0.0 && ns > 0.0) {
+          const double a = dot / sqrt(nx);
+          const double n1 = (double)al[0] + 1.0, dl = a - (double)al[1];
+          const double mean1 = (double)al[1] + dl / n1;
+          al[2] = (float)((double)al[2] + dl * (a - mean1));
+          al[1] = (float)mean1;
+          al[0] = (float)n1;
+        }
+      }
+    }
+    if (tid == 0) al[3] += 1.0f;
+  }
   if (tid == 0) {
     st_out[0] = (float)sm.dd;
     st_out[1] = (float)sm.dc;
@@ -470,11 +532,12 @@ __global__ __launch_bounds__(RF_NT) void k_reflex_feedback(
 sr_status launch_reflex_feedback(const sr_reflex_desc& d, const void* target_logits, const int32_t* p_row,
                                  const float* head_logits, const int32_t* q_row, const int32_t* cand,
                                  const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
-                                 float* memory, float* stats, float* e_out, hipStream_t s) {
+                                 float* memory, float* stats, float* e_out, const float* P, const float* rec_sketch,
+                                 float* align, hipStream_t s) {
 #define SR_RF_LAUNCH(TP, TW)                                                                                   \
   SR_LAUNCH("sr_reflex_feedback", (k_reflex_feedback<TP, TW>), dim3(d.R), dim3(RF_NT), 0, s,                  \
             (const TP*)target_logits, p_row, head_logits, q_row, cand, y_star, traj, horizon, (const TW*)W,     \
-            memory, stats, e_out, d)
+            memory, stats, e_out, P, rec_sketch, align, d)
   if (d.p_dtype == SR_BF16 && d.w_dtype == SR_BF16) {
     SR_RF_LAUNCH(bf16_t, bf16_t);
   } else if (d.p_dtype == SR_BF16) {
@@ -485,6 +548,119 @@ sr_status launch_reflex_feedback(const sr_reflex_desc& d, const void* target_log
     SR_RF_LAUNCH(float, float);
   }
 #undef SR_RF_LAUNCH
+  return SR_OK;
+}
+
+// ============================================================================ gated correction
+// One block per (trajectory, head) row: RMS of z and of the memory, the memory sketch, the reliability
+// gate from the alignment moments, and z + alpha RMS(z) m / (RMS(m) + eps) in place (rows the gate keeps
+// closed are not written).
+constexpr int RC_NT = 256;
+constexpr int RC_NW = RC_NT / 64;
+constexpr int RC_MAXE = 32;               // d <= RC_NT * RC_MAXE
+
+template <typename T>
+__global__ __launch_bounds__(RC_NT) void k_reflex_correct(T* __restrict__ z, const float* __restrict__ memory,
+                                                          const float* __restrict__ align, const float* __restrict__ P,
+                                                          float* __restrict__ sketch_out, float* __restrict__ alpha_out,
+                                                          int H, int d, sr_reflex_gate_desc g) {
+  __shared__ double red[RC_NW][2];
+  __shared__ double tot[RF_MAXS + 2];
+  __shared__ __attribute__((aligned(16))) float ms[RC_NT * RC_MAXE];     // the memory row, for the sketch
+  const int row = blockIdx.x, h = row % H;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  T* zr = z + (size_t)row * d;
+  const float* mr = memory + (size_t)row * d;
+  float zv[RC_MAXE], mv[RC_MAXE];
+  double sz = 0.0, sm2 = 0.0;
+#pragma unroll
+  for (int k = 0; k < RC_MAXE; ++k) {
+    const int c = tid + k * RC_NT;
+    zv[k] = 0.f;
+    mv[k] = 0.f;
+    if (c < d) {
+      zv[k] = Elem<T>::load(zr, c);
+      mv[k] = mr[c];
+      ms[c] = mv[k];
+    }
+    sz += (double)zv[k] * zv[k];
+    sm2 += (double)mv[k] * mv[k];
+  }
+  sz = wave_sum_f64(sz);
+  sm2 = wave_sum_f64(sm2);
+  if (lane == 0) { red[wave][0] = sz; red[wave][1] = sm2; }
+  __syncthreads();
+  // sketch rows j = wave, wave + RC_NW, ...: each lane walks the row with all of its wave's rows at once
+  const int rk = g.rank;
+  constexpr int JPW = (RF_MAXS + RC_NW - 1) / RC_NW;
+  float acc[JPW];
+#pragma unroll
+  for (int jj = 0; jj < JPW; ++jj) acc[jj] = 0.f;
+  // four consecutive columns per lane and step, several steps' loads in flight (d is a multiple of 8)
+#pragma unroll 4
+  for (int c = 4 * lane; c < d; c += 256) {
+    const f32x4 mc = *(const f32x4*)(ms + c);
+#pragma unroll
+    for (int jj = 0; jj < JPW; ++jj) {
+      const int j = wave + jj * RC_NW;
+      if (j < rk) {
+        const f32x4 pv = *(const f32x4*)(P + (size_t)j * d + c);
+        acc[jj] = fmaf(pv[0], mc[0], fmaf(pv[1], mc[1], fmaf(pv[2], mc[2], fmaf(pv[3], mc[3], acc[jj]))));
+      }
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < JPW; ++jj) {
+    const int j = wave + jj * RC_NW;
+    if (j < rk) {                               // uniform over the wave
+      const double v = wave_sum_f64((double)acc[jj]);
+      if (lane == 0) tot[2 + j] = v;
+    }
+  }
+  if (tid < 2) {
+    double a = 0.0;
+    for (int w = 0; w < RC_NW; ++w) a += red[w][tid];
+    tot[tid] = a;
+  }
+  __syncthreads();
+  const double rms_z = sqrt(tot[0] / d), rms_m = sqrt(tot[1] / d);
+  const float* al = align + (size_t)row * 4;
+  const double n = al[0], mean = al[1], m2 = al[2], nfb = al[3];
+  bool gate = n >= 2.0 && n >= (double)g.n_align_min[h] && nfb >= (double)g.n_fb_min[h] && rms_m > (double)g.m_floor;
+  double rel = 0.0;
+  if (gate) {
+    rel = mean - (double)g.z_delta * sqrt(m2 / (n - 1.0)) / sqrt(n);
+    gate = rel > 0.0;
+  }
+  const double alpha = gate ? (double)g.alpha_min[h] + ((double)g.alpha_max[h] - (double)g.alpha_min[h]) * fmin(rel, 1.0)
+                            : 0.0;
+  if (gate) {
+    const double coef = alpha * rms_z / (rms_m + (double)g.eps);
+#pragma unroll
+    for (int k = 0; k < RC_MAXE; ++k) {
+      const int c = tid + k * RC_NT;
+      if (c < d) Elem<T>::store(zr, c, (float)((double)zv[k] + coef * (double)mv[k]));
+    }
+  }
+  if (tid == 0 && alpha_out != nullptr) alpha_out[row] = (float)alpha;
+  if (sketch_out != nullptr && rk > 0) {
+    double nrm = 0.0;
+    for (int j = 0; j < rk; ++j) nrm += tot[2 + j] * tot[2 + j];
+    nrm = sqrt(nrm);
+    for (int j = tid; j < rk; j += RC_NT) sketch_out[(size_t)row * rk + j] = nrm > 0.0 ? (float)(tot[2 + j] / nrm) : 0.f;
+  }
+}
+
+sr_status launch_reflex_correct(const sr_heads_desc& d, const sr_reflex_gate_desc& g, void* z, const float* memory,
+                                const float* align, const float* P, float* sketch_out, float* alpha_out,
+                                hipStream_t s) {
+  if (d.dtype == SR_BF16) {
+    SR_LAUNCH("sr_reflex_correct", k_reflex_correct<bf16_t>, dim3(d.B * d.H), dim3(RC_NT), 0, s, (bf16_t*)z, memory,
+              align, P, sketch_out, alpha_out, d.H, d.d, g);
+  } else {
+    SR_LAUNCH("sr_reflex_correct", k_reflex_correct<float>, dim3(d.B * d.H), dim3(RC_NT), 0, s, (float*)z, memory,
+              align, P, sketch_out, alpha_out, d.H, d.d, g);
+  }
   return SR_OK;
 }
 

@@ -9,6 +9,11 @@ namespace sr {
 sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
                        const void* A, const void* bias, const void* W, float* x, void* n, void* z,
                        float* logits, float* gmax, hipStream_t s);
+// the two halves of launch_heads: clip + LayerNorm + head GEMM (z), then the vocabulary GEMM (+ group maxima)
+sr_status launch_heads_z(const sr_heads_desc& d, const void* hidden, const float* corr, const uint8_t* active,
+                         const void* A, const void* bias, float* x, void* n, void* z, hipStream_t s);
+sr_status launch_vocab(const sr_heads_desc& d, const void* z, const void* W, float* logits, float* gmax,
+                       hipStream_t s);
 // per-row maxima of the 64-column groups of fp32 logits [B*H, V]
 size_t group_max_count(const sr_heads_desc& d);
 sr_status launch_group_max(const sr_heads_desc& d, const float* logits, float* gmax, hipStream_t s);
@@ -48,6 +53,10 @@ sr_status launch_commit_path(const sr_commit_desc& d, const int32_t* acc_nodes, 
 sr_status launch_reflex_feedback(const sr_reflex_desc& d, const void* target_logits, const int32_t* p_row,
                                  const float* head_logits, const int32_t* q_row, const int32_t* cand,
                                  const int32_t* y_star, const int32_t* traj, const int32_t* horizon, const void* W,
-                                 float* memory, float* stats, float* e_out, hipStream_t s);
+                                 float* memory, float* stats, float* e_out, const float* P, const float* rec_sketch,
+                                 float* align, hipStream_t s);
+sr_status launch_reflex_correct(const sr_heads_desc& d, const sr_reflex_gate_desc& g, void* z, const float* memory,
+                                const float* align, const float* P, float* sketch_out, float* alpha_out,
+                                hipStream_t s);
 
 }  // namespace sr

@@ -29,6 +29,7 @@ _TID = {
     "hlogits": 50,
     "ckc": 60, "cvc": 61, "ckt": 62, "cvt": 63, "cacc": 64, "cperm": 65,
     "rp": 70, "rq": 71, "rcand": 72, "rslot": 73, "rmem": 74, "ry": 75, "rW": 76,
+    "gP": 80, "gmem": 81, "gsk": 82,
 }
 
 
@@ -474,3 +475,28 @@ def reflex_inputs(cfg: Config, seed: int = 0, R: Optional[int] = None, support: 
     if with_W:
         out["W"] = as_dtype(normal(_rng(seed, cfg, "rW"), (V, d), 0.02), cfg.dtype)
     return out
+
+
+def reflex_gate_inputs(cfg: Config, seed: int = 0, rank: int = 24) -> dict:
+    """Reflex state for the gated correction: memory ~ N(0, 0.1) per (trajectory, head) (one row all zero),
+    a projection P [rank, d] with unit rows, and alignment statistics (count, mean, M2, feedback count)
+    cycling through five cases per (trajectory, head) slot: enough aligned evidence (gate open), too few
+    observations, a negative mean, no feedback yet, and strong evidence (Rel near 1)."""
+    B, H, d = cfg.B, cfg.H, cfg.d
+    mem = normal(_rng(seed, cfg, "gmem"), (B, H, d), 0.1)
+    mem[0, H - 1] = 0.0
+    P = normal(_rng(seed, cfg, "gP"), (rank, d), 1.0)
+    P /= np.sqrt((P.astype(np.float64) ** 2).sum(axis=1, keepdims=True)).astype(np.float32)
+    cases = [(60, 0.5, 59 * 0.04, 10), (3, 0.5, 2 * 0.04, 10), (60, -0.1, 59 * 0.04, 10), (60, 0.5, 59 * 0.04, 0),
+             (100, 0.95, 99 * 0.0025, 20)]
+    align = np.array([cases[k % len(cases)] for k in range(B * H)], dtype=np.float32).reshape(B, H, 4)
+    return dict(memory=mem, P=P.astype(np.float32), align=align)
+
+
+def unit_sketches(n: int, rank: int, seed: int = 0, zero_every: int = 4) -> np.ndarray:
+    """Stored memory sketches: random unit vectors, every ``zero_every``-th row all zero (no sketch)."""
+    rng = np.random.default_rng(np.random.SeedSequence([int(seed), _TID["gsk"]]))
+    s = rng.standard_normal((n, rank))
+    s /= np.linalg.norm(s, axis=1, keepdims=True)
+    s[::zero_every] = 0.0
+    return s.astype(np.float32)

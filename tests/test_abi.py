@@ -39,7 +39,8 @@ def test_struct_layouts_match_header():
     assert C.sizeof(_lib.AcceptDesc) == 6 * 4
     assert C.sizeof(_lib.CommitDesc) == 10 * 4
     assert C.sizeof(_lib.BudgetDesc) == 4 * 4 + C.sizeof(C.c_void_p)
-    assert C.sizeof(_lib.ReflexDesc) == (12 + 7 + 8) * 4
+    assert C.sizeof(_lib.ReflexDesc) == (12 + 7 + 8 + 1) * 4
+    assert C.sizeof(_lib.ReflexGateDesc) == (4 + 8 * 4) * 4
 
 
 def _call_heads(desc, **ptrs):
@@ -166,7 +167,7 @@ def test_tree_budget_rejections():
 
 def _reflex_desc(**over):
     d = _lib.ReflexDesc(4, 512, 256, 2, 2, 4, 4, 3, 48, 4, _lib.SR_F32, _lib.SR_F32, 1.0, 0.15, 1.25, 0.3, 0.7,
-                        0.03, 1e-6, (C.c_float * 8)(0.85, 0.9, 0.95, 0.95, 0.95, 0.95, 0.95, 0.95))
+                        0.03, 1e-6, (C.c_float * 8)(0.85, 0.9, 0.95, 0.95, 0.95, 0.95, 0.95, 0.95), 0)
     for k, v in over.items():
         setattr(d, k, v)
     return d
@@ -178,7 +179,8 @@ def _reflex_desc(**over):
                                          ("w_cov", -1.0), ("n_p_rows", 0)])
 def test_reflex_descriptor_rejected(field, value):
     fake = C.c_void_p(1 << 20)
-    st = _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc(**{field: value})), *([fake] * 11), None, None)
+    st = _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc(**{field: value})), *([fake] * 11), None, None, None,
+                                       None, None)
     assert st == _lib.SR_ERR_INVALID
     assert _lib.last_error()
 
@@ -187,10 +189,40 @@ def test_reflex_rho_and_pointer_checks():
     fake = C.c_void_p(1 << 20)
     d = _reflex_desc()
     d.rho[1] = 1.0
-    assert _lib.lib().sr_reflex_feedback(C.byref(d), *([fake] * 11), None, None) == _lib.SR_ERR_INVALID
+    tail = (None, None, None, None, None)
+    assert _lib.lib().sr_reflex_feedback(C.byref(d), *([fake] * 11), *tail) == _lib.SR_ERR_INVALID
     args = [fake] * 11
     args[9] = None                                           # memory
-    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, None, None) == _lib.SR_ERR_INVALID
+    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, *tail) == _lib.SR_ERR_INVALID
     args = [fake] * 11
     args[8] = C.c_void_p((1 << 20) + 4)                      # misaligned W
-    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, None, None) == _lib.SR_ERR_INVALID
+    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc()), *args, *tail) == _lib.SR_ERR_INVALID
+    # alignment with rank > 0 needs P and the stored sketches
+    assert _lib.lib().sr_reflex_feedback(C.byref(_reflex_desc(rank=24)), *([fake] * 11), None, None, None, fake,
+                                         None) == _lib.SR_ERR_INVALID
+
+
+@pytest.mark.parametrize("change", ["rank", "eps", "alpha", "count", "H", "P"])
+def test_heads_reflex_gate_rejected(change):
+    hd = _lib.HeadsDesc(2, 256, 2, 512, 8, 2, _lib.SR_F32, 1.0, 1e-5)
+    g = sr.reflex_gate_desc(rank=4)
+    fake = C.c_void_p(1 << 20)
+    P = fake
+    if change == "rank":
+        g.rank = 65
+    elif change == "eps":
+        g.eps = 0.0
+    elif change == "alpha":
+        g.alpha_min[1] = 0.5
+    elif change == "count":
+        g.n_fb_min[0] = -1
+    elif change == "H":
+        hd.H = 9
+        hd.max_children = 2
+    else:
+        P = None
+    need = _lib.lib().sr_heads_propose_workspace(C.byref(_lib.HeadsDesc(2, 256, 2, 512, 8, 2, _lib.SR_F32, 1.0, 1e-5)))
+    st = _lib.lib().sr_heads_propose_reflex(C.byref(hd), C.byref(g), *([fake] * 9), fake, fake, P, None, None,
+                                            fake, fake, None, None, fake, need, None)
+    assert st == _lib.SR_ERR_INVALID, change
+    assert _lib.last_error()

@@ -170,3 +170,117 @@ def test_gate_duplicates_and_invalid_records():
     for i in range(cfg.B):
         for h in range(cfg.H):
             np.testing.assert_allclose(gm[i, h], om[i, h], rtol=1e-5, atol=1e-6)
+
+
+# ----------------------------------------------------------------------------- gated correction
+GATE = dict(z_delta=0.6, eps=1e-6, m_floor=1e-8, alpha_min=(0.010, 0.004, 0.0025), alpha_max=(0.025, 0.010, 0.006),
+            n_fb_min=(1, 2, 4), n_align_min=(6, 16, 48))
+
+
+def _per_head(v, h):
+    return v[min(h, len(v) - 1)]
+
+
+def _gpu_heads_reflex(inp, gin, P=True):
+    cfg = inp["cfg"]
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    B, H, V, d = cfg.B, cfg.H, cfg.V, cfg.d
+    rank = gin["P"].shape[0]
+    logits = torch.empty((B, H, V), dtype=torch.float32, device="cuda")
+    z = torch.empty((B, H, d), dtype=dt, device="cuda")
+    sk = torch.empty((B, H, rank), dtype=torch.float32, device="cuda")
+    al = torch.empty((B, H), dtype=torch.float32, device="cuda")
+    tok, cl = sr.heads_propose_reflex(dev_tensor(inp["hidden"]), dev_tensor(inp["corr"]), dev_tensor(inp["active"]),
+                                      dev_tensor(inp["A"]), dev_tensor(inp["bias"]), dev_tensor(inp["W"]),
+                                      dev_tensor(inp["parents"]), dev_tensor(inp["root_token"]),
+                                      dev_tensor(inp["u_tree"]), inp["max_children"], dev_tensor(gin["memory"]),
+                                      dev_tensor(gin["align"]), dev_tensor(gin["P"]), clip_norm=cfg.clip_norm,
+                                      logits=logits, z=z, sketch_out=sk, alpha_out=al, **GATE)
+    torch.cuda.synchronize()
+    return (tok.cpu().numpy(), cl.cpu().numpy(), logits.cpu().numpy(), z.float().cpu().numpy(), sk.cpu().numpy(),
+            al.cpu().numpy())
+
+
+@pytest.mark.parametrize("name,over", [("tiny-fp32", None), ("1.5B-shape", dict(B=5, V=20000))])
+def test_gated_correction_parity(name, over):
+    from helpers import assert_faithful_bf16, f64
+    cfg = synth.CONFIGS[0] if over is None else synth.scaled(synth.CONFIGS[1], **over)
+    inp = synth.heads_inputs(cfg, seed=7)
+    gin = synth.reflex_gate_inputs(cfg, seed=7)
+    print(f"[reflex-gate] {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} V={cfg.V}", flush=True)
+    tok, cl, lg, z, sk, alpha = _gpu_heads_reflex(inp, gin)
+    dt = cfg.dtype
+    ref = oracle.heads_forward(f64(inp["hidden"], dt), inp["corr"], inp["active"], f64(inp["A"], dt),
+                               f64(inp["bias"], dt), f64(inp["W"], dt), cfg.clip_norm, 1e-5,
+                               round_fn=None if dt == "f32" else oracle.round_bf16)
+    W64 = f64(inp["W"], dt)
+    opened = 0
+    for b in range(cfg.B):
+        for h in range(cfg.H):
+            st = tuple(float(x) for x in gin["align"][b, h, :3])
+            zt, a, _ = oracle.correction(ref["z"][b, h], gin["memory"][b, h], st, float(gin["align"][b, h, 3]),
+                                         _per_head(GATE["alpha_min"], h), _per_head(GATE["alpha_max"], h),
+                                         _per_head(GATE["n_fb_min"], h), _per_head(GATE["n_align_min"], h),
+                                         GATE["z_delta"], GATE["eps"], GATE["m_floor"])
+            opened += a > 0
+            assert alpha[b, h] == pytest.approx(a, abs=1e-7), (b, h)
+            s = oracle.sketch(gin["memory"][b, h], gin["P"])
+            np.testing.assert_allclose(sk[b, h], np.zeros(sk.shape[2]) if s is None else s, rtol=1e-5, atol=1e-6)
+            if dt == "f32":
+                assert row_rel_err(z[b, h], zt) <= 1e-5
+                zr = zt
+            else:
+                assert_faithful_bf16(z[b, h][None], zt[None])
+                zr = oracle.round_bf16(zt)
+            assert row_rel_err(lg[b, h], W64 @ zr) <= (1e-5 if dt == "f32" else 2e-3)
+    assert 0 < opened < cfg.B * cfg.H
+
+
+def test_closed_gates_match_plain_proposal():
+    cfg = synth.scaled(synth.CONFIGS[1], B=3, V=8000)
+    inp = synth.heads_inputs(cfg, seed=8)
+    gin = synth.reflex_gate_inputs(cfg, seed=8)
+    gin["align"][:, :, 3] = 0.0                     # no feedback yet: every gate closed
+    tok, cl, lg, z, sk, alpha = _gpu_heads_reflex(inp, gin)
+    assert (alpha == 0).all()
+    B, H, V, d = cfg.B, cfg.H, cfg.V, cfg.d
+    logits = torch.empty((B, H, V), dtype=torch.float32, device="cuda")
+    zz = torch.empty((B, H, d), dtype=torch.bfloat16, device="cuda")
+    tok2, cl2 = sr.heads_propose(dev_tensor(inp["hidden"]), dev_tensor(inp["corr"]), dev_tensor(inp["active"]),
+                                 dev_tensor(inp["A"]), dev_tensor(inp["bias"]), dev_tensor(inp["W"]),
+                                 dev_tensor(inp["parents"]), dev_tensor(inp["root_token"]), dev_tensor(inp["u_tree"]),
+                                 inp["max_children"], clip_norm=cfg.clip_norm, logits=logits, z=zz)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(tok, tok2.cpu().numpy())
+    np.testing.assert_array_equal(cl, cl2.cpu().numpy())
+    np.testing.assert_array_equal(lg, logits.cpu().numpy())
+    np.testing.assert_array_equal(z, zz.float().cpu().numpy())
+
+
+def test_feedback_alignment_moments():
+    cfg = synth.scaled(synth.CONFIGS[1], B=6, H=3)
+    inp = synth.reflex_inputs(cfg, seed=9)
+    gin = synth.reflex_gate_inputs(cfg, seed=9)
+    s_rec = synth.unit_sketches(inp["R"], gin["P"].shape[0], seed=9)
+    align0 = gin["align"].copy()
+    print(f"[reflex-align] {cfg.name} R={inp['R']}", flush=True)
+    mem = dev_tensor(inp["memory"])
+    al = dev_tensor(align0)
+    stats, e = sr.reflex_feedback(dev_tensor(inp["p_logits"]), dev_tensor(inp["p_row"]), dev_tensor(inp["q_logits"]),
+                                  dev_tensor(inp["q_row"]), dev_tensor(inp["cand"]), dev_tensor(inp["y_star"]),
+                                  dev_tensor(inp["traj"]), dev_tensor(inp["horizon"]), dev_tensor(inp["W"]), mem,
+                                  rho=RHO, want_e=True, P=dev_tensor(gin["P"]), rec_sketch=dev_tensor(s_rec), align=al,
+                                  support=inp["support"])
+    torch.cuda.synchronize()
+    om, info, oal = oracle.reflex_feedback(_Rows(inp["p_logits"], "bf16"), inp["p_row"], inp["q_logits"], inp["q_row"],
+                                           inp["cand"], inp["y_star"], inp["traj"], inp["horizon"],
+                                           _Rows(inp["W"], "bf16"), inp["memory"], rho=RHO, support=inp["support"],
+                                           P=gin["P"], rec_sketch=s_rec, align=align0)
+    gal = al.cpu().numpy()
+    st = stats.cpu().numpy()
+    observed = 0
+    for r, f in enumerate(info):
+        assert int(st[r, 5]) == f["applied"]
+        observed += "alignment" in f
+    assert observed > 0
+    np.testing.assert_allclose(gal, oal, rtol=1e-5, atol=1e-6)
