@@ -12,7 +12,12 @@ fallback token is drawn from the final residual (Alg. "Exact node-wise tree
 verification"). App. B.3 proves the committed tokens follow the target law.
 
 Readings taken here:
-* Target distribution p_u = softmax(target_logits[u] / temperature).
+* Target distribution p_u = softmax(target_logits[u] / temperature), then, when top_p < 1, nucleus
+  truncation as the rollouts use it (App. C "Training protocol": temperature 1.0, nucleus threshold 0.95):
+  tokens are ranked by (logit desc, id asc) and the smallest prefix of that ranking whose mass reaches
+  top_p is kept (a token is kept iff the mass ranked before it is below top_p); p_u is renormalised on
+  it. The same law is used at every visited node and for the bonus token. The margin of the truncation
+  is the distance of top_p to the cumulative mass before and through the last kept token.
 * The draft distribution over the children of u is the softmax of their
   ``child_logit`` values (the head logits of the drafted tokens), restricted
   to the children not yet tried.
@@ -44,14 +49,28 @@ def inverse_cdf(r: np.ndarray, U: float):
     return v, min(target - lo, cum[v] - target) / S
 
 
-def _target_dist(logits_row: np.ndarray, temperature: float) -> np.ndarray:
-    s = np.asarray(logits_row, dtype=np.float64) / temperature
+def _target_dist(logits_row: np.ndarray, temperature: float, top_p: float = 1.0):
+    """(p_u, truncation margin); the margin is inf without truncation."""
+    row = np.asarray(logits_row, dtype=np.float64)
+    s = row / temperature
     e = np.exp(s - s.max())
-    return e / e.sum()
+    p = e / e.sum()
+    if top_p >= 1.0:
+        return p, np.inf
+    order = np.lexsort((np.arange(row.shape[0]), -row))      # logit desc, id asc
+    cum = np.cumsum(p[order])
+    before = cum - p[order]
+    n_keep = int(np.count_nonzero(before < top_p))
+    kept = order[:n_keep]
+    out = np.zeros_like(p)
+    out[kept] = p[kept] / p[kept].sum()
+    margin = min(top_p - before[n_keep - 1], cum[n_keep - 1] - top_p)
+    return out, abs(margin)
 
 
 def tree_accept_one(target_logits: np.ndarray, child_logit: np.ndarray, tokens: np.ndarray,
-                    parents: np.ndarray, u_acc: np.ndarray, u_fin: float, temperature: float = 1.0):
+                    parents: np.ndarray, u_acc: np.ndarray, u_fin: float, temperature: float = 1.0,
+                    top_p: float = 1.0):
     """One trajectory. target_logits [T,V]; the other arrays are [T].
 
     Returns dict(acc_nodes, out_tokens, kind, margin, slot_margins).
@@ -61,7 +80,9 @@ def tree_accept_one(target_logits: np.ndarray, child_logit: np.ndarray, tokens: 
     acc_nodes, out_tokens, margins = [], [], []
     u = 0
     while True:
-        p = _target_dist(target_logits[u], temperature)
+        p, tm = _target_dist(target_logits[u], temperature, top_p)
+        if top_p < 1.0:
+            margins.append(tm)
         r = p.copy()                                           # r_u^(0) = p_u
         ch = kids[u]
         accepted = None
@@ -91,7 +112,10 @@ def tree_accept_one(target_logits: np.ndarray, child_logit: np.ndarray, tokens: 
         if kids[accepted]:
             u = accepted
             continue
-        tok, mg = inverse_cdf(_target_dist(target_logits[accepted], temperature), u_fin)  # bonus at the leaf
+        pl, tm = _target_dist(target_logits[accepted], temperature, top_p)
+        if top_p < 1.0:
+            margins.append(tm)
+        tok, mg = inverse_cdf(pl, u_fin)                       # bonus at the leaf
         margins.append(mg)
         out_tokens.append(tok)
         kind = BONUS
@@ -101,7 +125,7 @@ def tree_accept_one(target_logits: np.ndarray, child_logit: np.ndarray, tokens: 
 
 
 def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, temperature: float = 1.0,
-                max_depth: int = None, rows=None):
+                max_depth: int = None, rows=None, top_p: float = 1.0):
     """Batched wrapper with the library's output layout.
 
     target_logits [B,T,V] (float64 values), child_logit/tokens/parents/u_acc [B,T], u_fin [B].
@@ -119,7 +143,7 @@ def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, tempe
     margin = np.full(B, np.nan)
     for b in (range(B) if rows is None else rows):
         res = tree_accept_one(target_logits[b], child_logit[b], tokens[b], parents[b], u_acc[b],
-                              float(u_fin[b]), temperature)
+                              float(u_fin[b]), temperature, top_p)
         n = len(res["acc_nodes"])
         acc[b, :n] = res["acc_nodes"]
         outt[b, :n + 1] = res["out_tokens"]

@@ -242,3 +242,65 @@ def test_first_slot_closed_form_and_sandwich():
         acc = res[:, 1].mean()
         tol = 4.5 * math.sqrt(0.25 / N)
         assert pC * omega - tol <= acc <= pC + tol
+
+
+# ------------------------------------------------------------------- nucleus truncation of the target law
+def test_nucleus_hand_examples():
+    lg = np.log([0.5, 0.3, 0.15, 0.05])
+    p, _ = oracle.accept._target_dist(lg, 1.0, 0.79)       # mass before: 0, 0.5, 0.8 -> keep 2
+    np.testing.assert_allclose(p, [0.625, 0.375, 0.0, 0.0], rtol=1e-14)
+    p, _ = oracle.accept._target_dist(lg, 1.0, 0.81)       # 0.8 < 0.81 -> keep 3
+    np.testing.assert_allclose(p, [0.5 / 0.95, 0.3 / 0.95, 0.15 / 0.95, 0.0], rtol=1e-14)
+    # ties rank the lower id first: four equal logits, top_p 0.5 keeps ids 0 and 1
+    p, _ = oracle.accept._target_dist(np.zeros(4), 1.0, 0.5)
+    np.testing.assert_allclose(p, [0.5, 0.5, 0.0, 0.0], rtol=1e-14)
+    p, _ = oracle.accept._target_dist(np.array([0.0, 2.0, 0.0, 2.0]), 1.0, 0.6)
+    np.testing.assert_array_equal(p > 0, [False, True, False, True])
+    # top_p = 1 is the plain softmax
+    p1, m1 = oracle.accept._target_dist(lg, 1.0, 1.0)
+    np.testing.assert_allclose(p1, [0.5, 0.3, 0.15, 0.05], rtol=1e-14)
+    assert m1 == np.inf
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_nucleus_smallest_ranked_prefix(seed):
+    rng = np.random.default_rng(seed)
+    V = 40
+    lg = np.round(rng.standard_normal(V) * 2, 1)          # rounded: ties occur
+    base = np.exp(lg - lg.max())
+    base /= base.sum()
+    rank = sorted(range(V), key=lambda v: (-lg[v], v))
+    prev = 0
+    for top_p in (0.3, 0.6, 0.9, 0.95, 0.999):
+        p, _ = oracle.accept._target_dist(lg, 1.0, top_p)
+        kept = [v for v in rank if p[v] > 0]
+        n = len(kept)
+        assert kept == rank[:n]                            # a prefix of the ranking
+        assert base[kept].sum() >= top_p - 1e-12           # reaches top_p ...
+        assert base[kept[:-1]].sum() < top_p               # ... and no shorter prefix does
+        np.testing.assert_allclose(p[kept], base[kept] / base[kept].sum(), rtol=1e-13)
+        assert n >= prev                                   # grows with top_p
+        prev = n
+
+
+def test_nucleus_one_node_exactness():
+    """The committed token of one node follows the truncated target law (the exactness argument holds for
+    any target distribution): p = (1/2, 1/4, 1/8, 1/8) at top_p 0.7 keeps tokens 0 and 1 with (2/3, 1/3)."""
+    p = [0.5, 0.25, 0.125, 0.125]
+    cand = [1, 2, 3]
+    w = [3.0, 2.0, 1.0]
+    N = 30000
+    tl = np.tile(np.log(p), (len(cand) + 1, 1))
+    parents = np.array([-1] + [0] * len(cand))
+    head = np.full((1, 1, 4), -1e30)
+    head[0, 0, cand] = np.log(w)
+    rng = np.random.default_rng(23)
+    counts = np.zeros(4)
+    for n in range(N):
+        u = synth.uniforms(rng, (2 * len(cand) + 3,))
+        tok, cl, _ = oracle.tree_build(head, parents[None], np.array([0]), u[None, :len(cand) + 1])
+        res = oracle.tree_accept_one(tl, cl[0], tok[0], parents, u[len(cand) + 1:2 * len(cand) + 2], float(u[-1]),
+                                     top_p=0.7)
+        counts[res["out_tokens"][0]] += 1
+    assert counts[2] == 0 and counts[3] == 0
+    assert stats.chisquare(counts[:2], np.array([2 / 3, 1 / 3]) * N).pvalue > 0.01
