@@ -6,7 +6,8 @@ A step is the whole hot path over one batch of synthetic inputs resident in HBM:
   -> sr_tree_accept (exact acceptance walk).
 After the timed steps, the calls around the step are timed on their own and reported beside it: the
 accepted-path cache commit (sr_commit_path) of the last step's accepted paths for all 28 layers of the
-7B-shaped target, the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
+7B-shaped target, the acceptance walk with nucleus truncation (top_p 0.95, as the paper's rollouts
+sample), the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
 horizon) slot on the step's own target-logit rows, head logits and draft trees, and the gated head-state
 correction (the sr_reflex_correct kernel of sr_heads_propose_reflex) from the resulting memory.
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
@@ -199,6 +200,19 @@ def main():
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
     }
 
+    # the acceptance walk under the rollouts' nucleus truncation (top_p 0.95), same inputs
+    nouts = {k: torch.empty_like(v) for k, v in outs.items()}
+    for _ in range(2):
+        sr.tree_accept(C_["target_logits"], C_["child_logit"], C_["tokens"], C_["parents"], C_["u_acc"], C_["u_fin"],
+                       md, outputs=nouts, top_p=0.95)
+    torch.cuda.synchronize()
+    sr.prof_begin("sr_tree_accept")
+    for _ in range(10):
+        sr.tree_accept(C_["target_logits"], C_["child_logit"], C_["tokens"], C_["parents"], C_["u_acc"], C_["u_fin"],
+                       md, outputs=nouts, top_p=0.95)
+    nms, nn = sr.prof_end()
+    res["accept_top_p_0.95"] = {"avg_ms": nms / max(nn, 1), "launches": nn,
+                                "accepted_mean_len": float(nouts["out_len"].float().mean().item())}
     res["commit_path"] = commit_bench(sr, synth, cfg, args.seed, outs, dev)
     res["reflex_feedback"] = reflex_bench(sr, cfg, H, C_, hin, hws, dev)
     res["tree_budget"] = dict(zip(("N_t", "horizon_counts", "parents"), sr.tree_budget(B)))

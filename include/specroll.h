@@ -209,12 +209,20 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
  * U * S < sum_{w<=v} r(w). Walk scalars are float64; exponentials are fp32 of
  * (logit - running max) * (1/temperature), summed in float64.
  * The children of one node must carry distinct tokens.
+ * With top_p < 1 every p above (visited nodes and the bonus leaf) is first cut to
+ * its nucleus, as the paper's rollouts sample (App. C "Training protocol":
+ * nucleus threshold 0.95): tokens ranked by (logit desc, id asc) stay while the
+ * mass ranked before them is below top_p, and p is renormalised on them. Masses
+ * of the cut are fp32 exponentials summed in 40-bit fixed point; the cut's
+ * margin (distance of top_p to the cumulative mass around the last kept token)
+ * enters min_margin.
  */
 typedef struct {
   int32_t B, T, V;       /* trajectories; tree nodes (1..SR_MAX_TREE); vocabulary */
   int32_t max_depth;     /* columns of acc_nodes, >= the deepest node's depth    */
   sr_dtype logit_dtype;  /* element type of target_logits                        */
   float temperature;     /* > 0                                                  */
+  float top_p;           /* nucleus threshold in (0, 1]; 1 = no truncation       */
 } sr_accept_desc;
 
 size_t sr_tree_accept_workspace(const sr_accept_desc* desc);

@@ -194,9 +194,11 @@ def tree_verify_attn(q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, 
 
 
 def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, max_depth: int,
-                temperature: float = 1.0, outputs: Optional[dict] = None, want_margin: bool = True):
+                temperature: float = 1.0, outputs: Optional[dict] = None, want_margin: bool = True,
+                top_p: float = 1.0):
     """Exact acceptance walk. target_logits [B,T,V] bf16|f32; child_logit [B,T] f32; tokens, parents [B,T]
-    int32; u_acc [B,T] f32; u_fin [B] f32. Returns dict(acc_nodes, out_tokens, out_len, final_kind, min_margin)."""
+    int32; u_acc [B,T] f32; u_fin [B] f32; top_p < 1 cuts every target row to its nucleus.
+    Returns dict(acc_nodes, out_tokens, out_len, final_kind, min_margin)."""
     dev = target_logits.device
     B, T, V = target_logits.shape
     dt = target_logits.dtype
@@ -216,7 +218,7 @@ def tree_accept(target_logits, child_logit, tokens, parents, u_acc, u_fin, max_d
             final_kind=torch.empty((B,), dtype=torch.uint8, device=dev),
             min_margin=torch.empty((B,), dtype=torch.float32, device=dev) if want_margin else None,
         )
-    desc = AcceptDesc(B, T, V, int(max_depth), _DT[dt], float(temperature))
+    desc = AcceptDesc(B, T, V, int(max_depth), _DT[dt], float(temperature), float(top_p))
     st = lib().sr_tree_accept(C.byref(desc), _ptr(target_logits), _ptr(child_logit), _ptr(tokens), _ptr(parents),
                               _ptr(u_acc), _ptr(u_fin), _ptr(outputs["acc_nodes"]), _ptr(outputs["out_tokens"]),
                               _ptr(outputs["out_len"]), _ptr(outputs["final_kind"]), _ptr(outputs["min_margin"]),

@@ -32,7 +32,7 @@ class AttnDesc(C.Structure):
 
 class AcceptDesc(C.Structure):
     _fields_ = [("B", C.c_int32), ("T", C.c_int32), ("V", C.c_int32), ("max_depth", C.c_int32),
-                ("logit_dtype", C.c_int32), ("temperature", C.c_float)]
+                ("logit_dtype", C.c_int32), ("temperature", C.c_float), ("top_p", C.c_float)]
 
 
 class BudgetDesc(C.Structure):

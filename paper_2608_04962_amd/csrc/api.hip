@@ -311,6 +311,7 @@ static sr_status check_accept_desc(const sr_accept_desc* d) {
   SR_CHECK(d->max_depth >= 0 && d->max_depth <= SR_MAX_TREE, "max_depth must be in [0, %d]", SR_MAX_TREE);
   SR_CHECK(dtype_ok(d->logit_dtype), "unknown logit dtype %d", (int)d->logit_dtype);
   SR_CHECK(std::isfinite(d->temperature) && d->temperature > 0.f, "temperature must be finite and > 0");
+  SR_CHECK(d->top_p > 0.f && d->top_p <= 1.f, "top_p must be in (0, 1] (got %g)", (double)d->top_p);
   return SR_OK;
 }
 

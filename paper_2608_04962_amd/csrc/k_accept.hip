@@ -13,6 +13,15 @@
 // children (float64) plus one scalar for the mass outside them; the slot tests and the
 // normaliser Z are exact restatements of the full-vocabulary update. Terminal draws walk the
 // chunk sums, then one chunk, in token-id order.
+//
+// With nucleus truncation (top_p < 1) each target row is cut to the smallest prefix, in (logit desc, id
+// asc) order, whose mass reaches top_p: a radix select over the order-preserving keys of the logits with
+// histograms of the tokens' masses in 40-bit fixed point (integer sums: the same on every run), two
+// passes of 11 and 5 bits for bf16 rows and three of 11, 11 and 10 bits for fp32 rows, each counting only
+// tokens inside the bin chosen so far. All tokens of the final bin share one logit, so the number of
+// them that stay follows from their common mass; when the cut falls inside them, one more pass finds the
+// id of the last one kept. The walk then treats every token outside the nucleus as having zero mass; a
+// terminal draw first recomputes the chunk sums over the nucleus.
 #include <math.h>
 
 #include "common.hpp"
@@ -44,7 +53,12 @@ template <> struct RowLoad<float> {
   static __device__ __forceinline__ float load1(const float* p) { return *p; }
 };
 
+constexpr int NUC_NB = 2048;                 // bins of the first (widest) radix digit
+constexpr double NUC_FP = 1099511627776.0;   // 2^40: fixed-point scale of a token's mass (<= 1)
+
 struct AccSmem {
+  unsigned long long nh[NUC_NB];             // nucleus radix histogram (fixed-point masses)
+  int tie_cnt[ACC_MAX_CHUNKS];
   TreeLds<SR_MAX_TREE> tree;
   int tok[SR_MAX_TREE];
   float cl[SR_MAX_TREE];
@@ -59,7 +73,24 @@ struct AccSmem {
   int accepted;      // slot index (0-based) accepted at the current node, -1 = all rejected
   int draw_tok;
   double draw_margin;
+  float M;           // row max of logit / temperature
+  int nk_on;         // the nucleus cut is active for the current row
+  uint32_t nk_key;   // last kept key ...
+  int nk_idcut;      // ... and, among the tokens with that key, the last kept id
+  double nk_margin;
+  unsigned long long nk_above, nk_bin;
+  int nk_b;
 };
+
+__device__ __forceinline__ uint32_t acc_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ bool nuc_member(const AccSmem& sm, float x, int v) {
+  if (!sm.nk_on) return true;
+  const uint32_t k = acc_key(x);
+  return k > sm.nk_key || (k == sm.nk_key && v <= sm.nk_idcut);
+}
 
 // exp(y - m) with y = x * invtau, as 2^((y - m) log2 e) on the hardware exponential; every step is
 // rounded separately, so the value is identical wherever it is recomputed
@@ -110,7 +141,7 @@ __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float i
       sl += sm.csum[c] * sc;
     }
     const double S = wave_sum_f64(sl);
-    if (lane == 0) sm.S = S;
+    if (lane == 0) { sm.S = S; sm.M = M; sm.nk_on = 0; }
   }
   __syncthreads();
 }
@@ -120,8 +151,243 @@ template <typename T>
 __device__ __forceinline__ double ptilde(const AccSmem& sm, const T* row, int v, float invtau) {
   const int c = v / ACC_CH;
   const float x = RowLoad<T>::load1(row + v);
-  if (x == -INFINITY) return 0.0;
+  if (x == -INFINITY || !nuc_member(sm, x, v)) return 0.0;
   return (double)tilt(x, invtau, sm.cmax[c]) * sm.cscale[c];
+}
+
+// ---- nucleus truncation
+__device__ __forceinline__ unsigned long long nuc_fixed(float w) { return (unsigned long long)((double)w * NUC_FP); }
+
+// Histogram of the fixed-point masses of the tokens whose key matches prefix under pmask, by key digit
+// (key >> sh) & dmask. Whole block.
+template <typename T>
+__device__ void nuc_hist(AccSmem& sm, const T* __restrict__ row, int V, float invtau, uint32_t prefix,
+                         uint32_t pmask, int sh, uint32_t dmask) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  const float M = sm.M;
+  for (int i = tid; i < NUC_NB; i += ACC_NT) sm.nh[i] = 0ull;
+  __syncthreads();
+  for (int c0 = wave * ACC_GROUP; c0 < nch; c0 += ACC_NW * ACC_GROUP) {
+    float x[ACC_GROUP][8];
+#pragma unroll
+    for (int gi = 0; gi < ACC_GROUP; ++gi) {
+      const int base = (c0 + gi) * ACC_CH + lane * 8;
+      if (c0 + gi < nch && base < V) {
+        RowLoad<T>::load8(row + base, x[gi]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[gi][e] = -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int gi = 0; gi < ACC_GROUP; ++gi)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xv = x[gi][e];
+        const uint32_t k = acc_key(xv);
+        if (xv != -INFINITY && (k & pmask) == prefix)
+          atomicAdd(&sm.nh[(k >> sh) & dmask], nuc_fixed(tilt(xv, invtau, M)));
+      }
+  }
+  __syncthreads();
+}
+
+// Wave 0: among bins [0, nb) in descending order, the bin b with above + (bins > b) < target <=
+// above + (bins >= b); sets sm.nk_b, sm.nk_above (mass ranked before the bin) and sm.nk_bin (its mass).
+__device__ void nuc_find(AccSmem& sm, int nb, unsigned long long above, unsigned long long target) {
+  const int lane = threadIdx.x & 63;
+  const int per = (nb + 63) / 64;                 // lane l owns bins nb-1-l*per down to nb-(l+1)*per
+  unsigned long long ls = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = nb - 1 - lane * per - j;
+    if (b >= 0) ls += sm.nh[b];
+  }
+  // exclusive prefix over lanes (lane 0 holds the top bins)
+  unsigned long long incl = ls;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  const unsigned long long before = above + (incl - ls);
+  const bool mine = before < target && target <= before + ls;
+  const unsigned long long bal = __ballot(mine);
+  const int owner = bal ? __ffsll((long long)bal) - 1 : 63;
+  if (lane == owner) {
+    unsigned long long cum = before;
+    int bsel = max(0, nb - 1 - lane * per - (per - 1));
+    unsigned long long msel = 0, asel = cum;
+    for (int j = 0; j < per; ++j) {
+      const int b = nb - 1 - lane * per - j;
+      if (b < 0) break;
+      const unsigned long long m = sm.nh[b];
+      if (cum < target && target <= cum + m) { bsel = b; msel = m; asel = cum; break; }
+      cum += m;
+    }
+    sm.nk_b = bsel;
+    sm.nk_above = asel;
+    sm.nk_bin = msel;
+  }
+}
+
+// The first `want` tokens (in id order) whose key equals kstar: the id of the last of them. Whole block;
+// the result is in sm.nk_idcut.
+template <typename T>
+__device__ void nuc_tie_cut(AccSmem& sm, const T* __restrict__ row, int V, uint32_t kstar, int want) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  for (int c = wave; c < nch; c += ACC_NW) {
+    const int base = c * ACC_CH + lane * 8;
+    int n = 0;
+    if (base < V) {
+      float x[8];
+      RowLoad<T>::load8(row + base, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) n += (x[e] != -INFINITY && acc_key(x[e]) == kstar) ? 1 : 0;
+    }
+    n = warp_sum_i(n);
+    if (lane == 0) sm.tie_cnt[c] = n;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    constexpr int CPL = ACC_MAX_CHUNKS / 64;
+    int cnt[CPL], ls = 0;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int c = lane * CPL + i;
+      cnt[i] = c < nch ? sm.tie_cnt[c] : 0;
+      ls += cnt[i];
+    }
+    int incl = ls;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    int before = incl - ls, cstar = -1, cbefore = 0;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (cstar < 0 && before < want && want <= before + cnt[i]) { cstar = lane * CPL + i; cbefore = before; }
+      before += cnt[i];
+    }
+    const unsigned long long bal = __ballot(cstar >= 0);
+    const int owner = bal ? __ffsll((long long)bal) - 1 : 0;
+    cstar = max(0, __shfl(cstar, owner, 64));
+    cbefore = __shfl(cbefore, owner, 64);
+    // scan the chunk: 8 tokens per lane
+    const int base = cstar * ACC_CH + lane * 8;
+    float x[8];
+    int n = 0;
+    if (base < V) {
+      RowLoad<T>::load8(row + base, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) n += (x[e] != -INFINITY && acc_key(x[e]) == kstar) ? 1 : 0;
+    }
+    int li = n;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(li, o, 64);
+      if (lane >= o) li += t;
+    }
+    int cum = cbefore + li - n, id = -1;
+    if (base < V) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (x[e] != -INFINITY && acc_key(x[e]) == kstar) {
+          ++cum;
+          if (cum == want && id < 0) id = base + e;
+        }
+      }
+    }
+    const unsigned long long b2 = __ballot(id >= 0);
+    const int idv = __shfl(id, b2 ? __ffsll((long long)b2) - 1 : 0, 64);
+    if (lane == 0 && b2) sm.nk_idcut = idv;
+  }
+  __syncthreads();
+}
+
+// Nucleus cut of the current row (after row_stats): membership fields of sm, sm.S = the nucleus mass and
+// sm.nk_margin. Whole block.
+template <typename T>
+__device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float invtau, float top_p) {
+  const int tid = threadIdx.x, wave = tid >> 6;
+  constexpr bool BF = sizeof(T) == 2;
+  constexpr int NP = BF ? 2 : 3;
+  const int shs[3] = {21, BF ? 16 : 10, 0};
+  const int bits[3] = {11, BF ? 5 : 11, 10};
+  uint32_t prefix = 0, pmask = 0;
+  unsigned long long above = 0, target = 0, total = 0;
+  for (int pass = 0; pass < NP; ++pass) {
+    const uint32_t dmask = (1u << bits[pass]) - 1u;
+    nuc_hist<T>(sm, row, V, invtau, prefix, pmask, shs[pass], dmask);
+    if (pass == 0) {
+      // total mass and the integer target: a token stays iff the mass ranked before it is < top_p * total
+      if (wave == 0) {
+        unsigned long long ls = 0;
+        for (int b = threadIdx.x; b < NUC_NB; b += 64) ls += sm.nh[b];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) ls += __shfl_xor(ls, o, 64);
+        if (threadIdx.x == 0) {
+          sm.nk_above = ls;                       // stash the total
+        }
+      }
+      __syncthreads();
+      total = sm.nk_above;
+      target = (unsigned long long)ceil((double)top_p * (double)total);
+      __syncthreads();
+    }
+    if (wave == 0) nuc_find(sm, 1 << bits[pass], above, target);
+    __syncthreads();
+    above = sm.nk_above;
+    prefix |= (uint32_t)sm.nk_b << shs[pass];
+    pmask |= dmask << shs[pass];
+    __syncthreads();
+  }
+  // every token of the final bin has one key and the same mass q. A bf16 value widened to fp32 has 16 zero
+  // low bits, so its key's low bits are all zero (positive) or all one (negative): complete the key.
+  if (BF && !(prefix & 0x80000000u)) prefix |= 0xffffu;
+  const unsigned long long bin_mass = sm.nk_bin;
+  // the mass of one such token, recomputed from its value
+  const uint32_t u = (prefix & 0x80000000u) ? (prefix & 0x7fffffffu) : ~prefix;
+  const float xk = __uint_as_float(u);
+  const unsigned long long q = nuc_fixed(tilt(xk, invtau, sm.M));
+  const unsigned long long n_tie = q > 0 ? bin_mass / q : 1;
+  // tokens t = 0.. of the bin stay while above + t q < target
+  const unsigned long long need = q > 0 ? (target - above + q - 1) / q : n_tie;
+  const unsigned long long kt = need < n_tie ? need : n_tie;
+  if (tid == 0) {
+    sm.nk_key = prefix;
+    sm.nk_idcut = 0x7fffffff;
+    const double bl = (double)(above + (kt - 1) * q), bh = bl + (double)q, tg = (double)top_p * (double)total;
+    sm.nk_margin = fmin(tg - bl, bh - tg) / (double)total;
+    sm.S = (double)(above + kt * q) / NUC_FP;
+  }
+  __syncthreads();
+  if (kt < n_tie) nuc_tie_cut<T>(sm, row, V, prefix, (int)kt);
+  if (tid == 0) sm.nk_on = 1;
+  __syncthreads();
+}
+
+// chunk sums restricted to the nucleus (for the terminal draws), relative to the chunk maxima
+template <typename T>
+__device__ void nuc_masked_sums(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  for (int c = wave; c < nch; c += ACC_NW) {
+    const int base = c * ACC_CH + lane * 8;
+    float sl = 0.f;
+    if (base < V) {
+      float x[8];
+      RowLoad<T>::load8(row + base, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (x[e] != -INFINITY && nuc_member(sm, x[e], base + e)) sl += tilt(x[e], invtau, sm.cmax[c]);
+    }
+    const float s = wave_sum_f32(sl);
+    if (lane == 0) sm.csum[c] = (double)s;
+  }
+  __syncthreads();
 }
 
 // Inverse-CDF draw over the current row, token-id order, excluding the tokens of
@@ -259,7 +525,8 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
                                                         const int32_t* __restrict__ parents,
                                                         const float* __restrict__ u_acc,
                                                         const float* __restrict__ u_fin, int T_, int V,
-                                                        int max_depth, float invtau, int32_t* __restrict__ acc_nodes,
+                                                        int max_depth, float invtau, float top_p,
+                                                        int32_t* __restrict__ acc_nodes,
                                                         int32_t* __restrict__ out_tokens,
                                                         int32_t* __restrict__ out_len, uint8_t* __restrict__ kind,
                                                         float* __restrict__ min_margin) {
@@ -305,6 +572,10 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   while (true) {
     const T* row = base + (size_t)u * V;
     row_stats<T>(sm, row, V, invtau);
+    if (top_p < 1.f) {
+      nucleus<T>(sm, row, V, invtau, top_p);
+      if (tid == 0) margin = fmin(margin, sm.nk_margin);
+    }
     if (tid == 0) {
       int n = 0;
       for (int c = u + 1; c < T_; ++c)
@@ -372,6 +643,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     const int acc = sm.accepted;
     if (acc < 0) {
       // every child rejected: fallback from the final residual = p outside the children
+      if (top_p < 1.f) nuc_masked_sums<T>(sm, row, V, invtau);
       if (wave == 0) draw<T>(sm, row, V, invtau, m, Ufin);
       __syncthreads();
       if (tid == 0) {
@@ -391,6 +663,11 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     // accepted leaf: bonus token from its own target distribution
     const T* lrow = base + (size_t)c * V;
     row_stats<T>(sm, lrow, V, invtau);
+    if (top_p < 1.f) {
+      nucleus<T>(sm, lrow, V, invtau, top_p);
+      if (tid == 0) margin = fmin(margin, sm.nk_margin);
+      nuc_masked_sums<T>(sm, lrow, V, invtau);
+    }
     if (wave == 0) draw<T>(sm, lrow, V, invtau, 0, Ufin);
     __syncthreads();
     if (tid == 0) {
@@ -412,11 +689,11 @@ sr_status launch_tree_accept(const sr_accept_desc& d, const void* target_logits,
   if (d.logit_dtype == SR_BF16) {
     SR_LAUNCH("sr_tree_accept", k_tree_accept<bf16_t>, dim3(d.B), dim3(ACC_NT), 0, s,
               (const bf16_t*)target_logits, child_logit, tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth,
-              invtau, acc_nodes, out_tokens, out_len, final_kind, min_margin);
+              invtau, d.top_p, acc_nodes, out_tokens, out_len, final_kind, min_margin);
   } else {
     SR_LAUNCH("sr_tree_accept", k_tree_accept<float>, dim3(d.B), dim3(ACC_NT), 0, s,
               (const float*)target_logits, child_logit, tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth,
-              invtau, acc_nodes, out_tokens, out_len, final_kind, min_margin);
+              invtau, d.top_p, acc_nodes, out_tokens, out_len, final_kind, min_margin);
   }
   return SR_OK;
 }

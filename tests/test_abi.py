@@ -36,7 +36,7 @@ def test_struct_layouts_match_header():
     # the descriptors are plain int32/float fields in header order
     assert C.sizeof(_lib.HeadsDesc) == 9 * 4
     assert C.sizeof(_lib.AttnDesc) == 10 * 4
-    assert C.sizeof(_lib.AcceptDesc) == 6 * 4
+    assert C.sizeof(_lib.AcceptDesc) == 7 * 4
     assert C.sizeof(_lib.CommitDesc) == 10 * 4
     assert C.sizeof(_lib.BudgetDesc) == 4 * 4 + C.sizeof(C.c_void_p)
     assert C.sizeof(_lib.ReflexDesc) == (12 + 7 + 8 + 1) * 4
@@ -86,9 +86,9 @@ def test_attn_descriptor_rejected(field, value):
 
 
 @pytest.mark.parametrize("field,value", [("V", 12), ("V", 1 << 20), ("temperature", 0.0), ("max_depth", -1),
-                                         ("T", 0)])
+                                         ("T", 0), ("top_p", 0.0), ("top_p", 1.5), ("top_p", float("nan"))])
 def test_accept_descriptor_rejected(field, value):
-    desc = _lib.AcceptDesc(2, 8, 512, 3, _lib.SR_F32, 1.0)
+    desc = _lib.AcceptDesc(2, 8, 512, 3, _lib.SR_F32, 1.0, 1.0)
     setattr(desc, field, value)
     st = _lib.lib().sr_tree_accept(C.byref(desc), *([None] * 11), None, 0, None)
     assert st == _lib.SR_ERR_INVALID
@@ -100,7 +100,7 @@ def test_workspace_queries_are_consistent():
     assert ws > 0 and ws % 256 == 0
     d1 = _lib.AttnDesc(2, 8, 4, 2, 64, 16, 10, 20, _lib.SR_F32, 0.125)   # one chunk: no partials
     assert _lib.lib().sr_tree_verify_attn_workspace(C.byref(d1)) == 0
-    assert _lib.lib().sr_tree_accept_workspace(C.byref(_lib.AcceptDesc(2, 8, 512, 3, 0, 1.0))) == 0
+    assert _lib.lib().sr_tree_accept_workspace(C.byref(_lib.AcceptDesc(2, 8, 512, 3, 0, 1.0, 1.0))) == 0
 
 
 def test_prof_hook_host_side():

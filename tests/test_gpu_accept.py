@@ -17,21 +17,22 @@ pytestmark = pytest.mark.gpu
 MARGIN = 1e-6   # decisions closer than this to their threshold may legitimately differ
 
 
-def _gpu_accept(inp, temperature=1.0):
+def _gpu_accept(inp, temperature=1.0, top_p=1.0):
     res = sr.tree_accept(dev_tensor(inp["target_logits"]), dev_tensor(inp["child_logit"]), dev_tensor(inp["tokens"]),
                          dev_tensor(inp["parents"]), dev_tensor(inp["u_acc"]), dev_tensor(inp["u_fin"]),
-                         inp["max_depth"], temperature)
+                         inp["max_depth"], temperature, top_p=top_p)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in res.items() if v is not None}
 
 
-def _compare(inp, rows=None, temperature=1.0):
+def _compare(inp, rows=None, temperature=1.0, top_p=1.0):
     cfg = inp["cfg"]
-    print(f"[accept] {cfg.name} B={cfg.B} T={cfg.T} V={cfg.V}", flush=True)
-    g = _gpu_accept(inp, temperature)
+    print(f"[accept] {cfg.name} B={cfg.B} T={cfg.T} V={cfg.V} top_p={top_p}", flush=True)
+    g = _gpu_accept(inp, temperature, top_p)
     rows = list(range(cfg.B)) if rows is None else [int(r) for r in rows]
     o = oracle.tree_accept(_Rows(inp["target_logits"], inp["dtype"]), inp["child_logit"], inp["tokens"],
-                           inp["parents"], inp["u_acc"], inp["u_fin"], temperature, inp["max_depth"], rows=rows)
+                           inp["parents"], inp["u_acc"], inp["u_fin"], temperature, inp["max_depth"], rows=rows,
+                           top_p=top_p)
     exempt = 0
     for b in rows:
         same = (np.array_equal(g["acc_nodes"][b], o["acc_nodes"][b])
@@ -116,10 +117,51 @@ def test_deterministic():
         np.testing.assert_array_equal(a[k], b[k])
 
 
+# ---------------------------------------------------------------- nucleus truncation
+@pytest.mark.parametrize("top_p", [0.95, 0.5])
+def test_nucleus_config0_and_scaled(top_p):
+    _compare(synth.accept_inputs(synth.CONFIGS[0], seed=10), top_p=top_p)
+    _compare(synth.accept_inputs(synth.scaled(synth.CONFIGS[2], B=48, V=4096), seed=11), top_p=top_p)
+
+
+def test_nucleus_deep_walks_and_temperature():
+    cfg = synth.scaled(synth.CONFIGS[1], B=64, V=1024, dtype="f32")
+    inp = synth.accept_inputs(cfg, seed=12, target_std=8.0, noise_std=0.05)
+    g, _ = _compare(inp, top_p=0.9)
+    assert (g["final_kind"] == 1).sum() > 0
+    _compare(synth.accept_inputs(synth.scaled(synth.CONFIGS[2], B=16, V=2048), seed=13), temperature=0.5, top_p=0.95)
+
+
+def test_nucleus_ties_cut_inside_equal_logits():
+    """Rows whose logits take few distinct values (the cut falls among equal logits and is decided by id),
+    a constant row and an all-negative row."""
+    cfg = synth.scaled(synth.CONFIGS[2], B=24, V=4096)
+    inp = synth.accept_inputs(cfg, seed=14)
+    tl = synth.to_f64(inp["target_logits"], "bf16")
+    tl = np.round(tl / 2.0) * 2.0                   # values on a coarse grid: heavy ties
+    tl[0] = 0.0
+    tl[1] = -np.abs(tl[1]) - 5.0
+    inp["target_logits"] = synth.as_dtype(tl.astype(np.float32), "bf16")
+    for top_p in (0.95, 0.37):
+        _compare(inp, top_p=top_p)
+    f32 = dict(inp, target_logits=tl.astype(np.float32), dtype="f32", cfg=synth.scaled(cfg, dtype="f32"))
+    _compare(f32, top_p=0.6)
+
+
+@pytest.mark.parametrize("cfg_id", [2, 3])
+def test_nucleus_full_size_sampled(cfg_id):
+    cfg = synth.CONFIGS[cfg_id]
+    inp = synth.accept_inputs(cfg, seed=1)
+    rows = np.random.default_rng(10 + cfg_id).choice(cfg.B, size=min(8, cfg.B), replace=False)
+    _compare(inp, rows=rows, top_p=0.95)
+
+
 # ---------------------------------------------------------------- exactness of the GPU path
-def test_gpu_chi_square_exactness_1e6():
+@pytest.mark.parametrize("top_p", [1.0, 0.8])
+def test_gpu_chi_square_exactness_1e6(top_p):
     """Tree build (sr_tree_build) + acceptance (sr_tree_accept), 1e6 independent trajectories with fresh
-    uniforms: the first committed token must follow p_root and the first two tokens p(x1) p(x2|x1)."""
+    uniforms: the first committed token must follow p_root and the first two tokens p(x1) p(x2|x1), where
+    p is the (nucleus-truncated, for top_p < 1) target law."""
     V, H, N = 8, 2, 1_000_000
     parents = np.array([-1, 0, 0, 0, 1, 1, 2], dtype=np.int32)       # root 3 slots; node 1: 2; node 2: 1
     T = parents.shape[0]
@@ -150,17 +192,17 @@ def test_gpu_chi_square_exactness_1e6():
     tl = tl.contiguous()
     u_acc = torch.rand((B, T), generator=g, device=dev).clamp_(1e-7, 1 - 1e-7)
     u_fin = torch.rand((B,), generator=g, device=dev).clamp_(1e-7, 1 - 1e-7)
-    res = sr.tree_accept(tl, cl, tok, par, u_acc, u_fin, max_depth=2)
+    res = sr.tree_accept(tl, cl, tok, par, u_acc, u_fin, max_depth=2, top_p=top_p)
     out = res["out_tokens"].cpu().numpy()
     olen = res["out_len"].cpu().numpy()
     assert (res["final_kind"].cpu().numpy() != 255).all()
-    b64 = base.astype(np.float64)
-    p0 = np.exp(b64 - b64.max()); p0 /= p0.sum()
+    p0, _ = oracle.accept._target_dist(base.astype(np.float64), 1.0, top_p)
     first = np.bincount(out[:, 0], minlength=V)
-    assert stats.chisquare(first, p0 / p0.sum() * N).pvalue > 0.01
+    assert (first[p0 == 0] == 0).all()
+    keep = p0 > 0
+    assert stats.chisquare(first[keep], p0[keep] * N).pvalue > 0.01
     # second token: where the round committed >= 2 tokens use it, else continue with a fresh draw from p(.|x1)
-    c64 = cond.astype(np.float64)
-    pc = np.exp(c64 - c64.max(1, keepdims=True)); pc /= pc.sum(1, keepdims=True)
+    pc = np.stack([oracle.accept._target_dist(cond[a].astype(np.float64), 1.0, top_p)[0] for a in range(V)])
     x1 = out[:, 0]
     x2 = out[:, 1].copy()
     need = olen < 2
@@ -169,5 +211,6 @@ def test_gpu_chi_square_exactness_1e6():
     x2[need] = (u2[:, None] * cdf[:, -1:] >= cdf).sum(1)
     joint = np.bincount(x1 * V + x2, minlength=V * V)
     exp = (p0[:, None] * pc).ravel()
+    assert (joint[exp == 0] == 0).all()
     exp = exp / exp.sum() * N
-    assert stats.chisquare(joint, exp).pvalue > 0.01
+    assert stats.chisquare(joint[exp > 0], exp[exp > 0]).pvalue > 0.01
