@@ -9,7 +9,9 @@ accepted-path cache commit (sr_commit_path) of the last step's accepted paths fo
 7B-shaped target, the acceptance walk with nucleus truncation (top_p 0.95, as the paper's rollouts
 sample), the Reflex feedback (sr_reflex_feedback) of one matured record per (trajectory,
 horizon) slot on the step's own target-logit rows, head logits and draft trees, and the gated head-state
-correction (the sr_reflex_correct kernel of sr_heads_propose_reflex) from the resulting memory.
+correction (the sr_reflex_correct kernel of sr_heads_propose_reflex) from the resulting memory. Finally the
+whole step is timed on the other workloads (1.5B-shaped, 14B-shaped tail, and the seven points of the
+7B-shaped concurrency sweep) and reported under "other_configs".
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
 hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
 
@@ -77,6 +79,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=32, help="trajectories the oracle runs on")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the step timings of the 1.5B, 14B and concurrency-sweep workloads")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run a plain 1 GiB float32 elementwise copy (negation) before the steps, as the "
                          "reference point that scales the HBM byte counters of a profiler run")
@@ -217,9 +221,99 @@ def main():
     res["reflex_feedback"] = reflex_bench(sr, cfg, H, C_, hin, hws, dev)
     res["tree_budget"] = dict(zip(("N_t", "horizon_counts", "parents"), sr.tree_budget(B)))
 
+    if not args.no_other_configs:
+        res["other_configs"] = other_configs(sr, synth, dev, W7=H["W"], A7=H["A"], bias7=H["bias"])
+
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, hin, ain, cin, args.cpu_sample)
     print(json.dumps(res), flush=True)
+
+
+def other_configs(sr, synth, dev, W7=None, A7=None, bias7=None, steps=5, warmup=2):
+    """Whole-step throughput of the other workloads: the 1.5B-shaped step, the 14B-shaped tail step and the
+    seven points of the 7B-shaped concurrency sweep (live batch 256 -> 4, tree 8 -> 96 nodes). Values are
+    drawn on the GPU with the workloads' distributions (only the timing is used); context lengths, trees and
+    page tables follow the same recipe as the main workload."""
+    import numpy as np
+    import torch
+    g = torch.Generator(device=dev).manual_seed(1)
+    bf = torch.bfloat16
+    rn = lambda shape, std: (torch.randn(shape, generator=g, device=dev) * std).to(bf)  # noqa: E731
+    cases = [("1.5B-shape", synth.CONFIGS[1]), ("14B-shape-tail", synth.CONFIGS[3])]
+    cases += [(f"7B-sweep-B{b}-T{t}", synth.sweep_config(b, t)) for b, t in synth.SWEEP_POINTS]
+    out = {}
+    for name, cfg in cases:
+        B, T, Hq, Hkv, D, d, Hh, V = cfg.B, cfg.T, cfg.Hq, cfg.Hkv, cfg.D, cfg.d, cfg.H, cfg.V
+        seven = d == 3584 and W7 is not None
+        W = W7 if seven else rn((V, d), 0.02)
+        A = A7 if seven else rn((Hh, d, d), 0.02)
+        bias = bias7 if seven else rn((Hh, d), 0.02)
+        hidden = rn((B, d), 1.0)
+        corr = torch.randn((B, d), generator=g, device=dev) * 0.1
+        active = (torch.rand((B,), generator=g, device=dev) < cfg.active_frac).to(torch.uint8)
+        par_np = synth.topology(cfg)
+        parents = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(par_np, (B, T)))).to(dev)
+        root = torch.randint(0, V, (B,), generator=g, device=dev, dtype=torch.int32)
+        u_tree = torch.rand((B, T), generator=g, device=dev).clamp_(1e-6, 1 - 1e-6)
+        mc = synth.max_children(par_np)
+        L = synth.context_lengths(cfg, 0)
+        nblk = -(-L // cfg.block_size)
+        NB = int(nblk.sum())
+        perm = np.random.default_rng(0).permutation(NB).astype(np.int32)
+        table = np.full((B, cfg.max_blocks), -1, dtype=np.int32)
+        off = 0
+        for b in range(B):
+            table[b, :nblk[b]] = perm[off:off + nblk[b]]
+            off += nblk[b]
+        q = rn((B, T, Hq, D), 1.0)
+        kc, vc = rn((NB, Hkv, cfg.block_size, D), 1.0), rn((NB, Hkv, cfg.block_size, D), 1.0)
+        kt, vt = rn((B, T, Hkv, D), 1.0), rn((B, T, Hkv, D), 1.0)
+        bt, cl_ = torch.from_numpy(table).to(dev), torch.from_numpy(L.astype(np.int32)).to(dev)
+        tl = rn((B, T, V), 4.0)
+        u_acc = torch.rand((B, T), generator=g, device=dev).clamp_(1e-6, 1 - 1e-6)
+        u_fin = torch.rand((B,), generator=g, device=dev).clamp_(1e-6, 1 - 1e-6)
+        md = int(synth.node_depths(par_np).max()) if T > 1 else 0
+        tok = torch.empty((B, T), dtype=torch.int32, device=dev)
+        cl = torch.empty((B, T), dtype=torch.float32, device=dev)
+        hws = torch.empty(sr.heads_workspace_bytes(B, d, Hh, V, T, mc), dtype=torch.uint8, device=dev)
+        o = torch.empty((B, T, Hq, D), dtype=torch.float32, device=dev)
+        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=dev)
+        adesc = sr.attn_desc(q, kc, bt)
+        aws = torch.empty(max(sr.attn_workspace_bytes(adesc), 1), dtype=torch.uint8, device=dev)
+        outs = dict(acc_nodes=torch.empty((B, max(md, 1)), dtype=torch.int32, device=dev),
+                    out_tokens=torch.empty((B, md + 1), dtype=torch.int32, device=dev),
+                    out_len=torch.empty((B,), dtype=torch.int32, device=dev),
+                    final_kind=torch.empty((B,), dtype=torch.uint8, device=dev),
+                    min_margin=torch.empty((B,), dtype=torch.float32, device=dev))
+
+        def step():
+            sr.heads_propose(hidden, corr, active, A, bias, W, parents, root, u_tree, mc, tokens=tok, child_logit=cl,
+                             workspace=hws)
+            sr.tree_verify_attn(q, kc, vc, bt, cl_, kt, vt, parents, out=o, lse=lse, workspace=aws)
+            sr.tree_accept(tl, cl, tok, parents, u_acc, u_fin, md, outputs=outs)
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        sr.prof_begin("sr_tree_attn")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ams, an = sr.prof_end()
+        ms = e0.elapsed_time(e1) / steps
+        kv = float(L.sum()) * 2 * Hkv * D * 2 + B * T * (Hq + 2 * Hkv) * D * 2 + B * T * Hq * (D + 1) * 4
+        am = ams / max(an, 1)
+        assert (outs["final_kind"].cpu() != 255).all(), name
+        out[name] = {"B": B, "T": T, "ms_per_step": ms, "tree_tokens_per_s": B * T / (ms / 1e3),
+                     "tree_attn_ms": am, "tree_attn_GB/s": kv / (am / 1e3) / 1e9}
+        log(f"{name}: {ms:.3f} ms/step, {B * T / (ms / 1e3):.4g} tree tokens/s, attention {kv / (am / 1e3) / 1e9:.0f} GB/s")
+        del q, kc, vc, kt, vt, tl
+        if not seven:
+            del W, A, bias
+        torch.cuda.empty_cache()
+    return out
 
 
 def commit_bench(sr, synth, cfg, seed, outs, dev):

@@ -29,7 +29,8 @@ constexpr int ATT_KT = 64;             // keys per LDS tile
 constexpr int ATT_NW = 8;              // waves per block
 constexpr int ATT_RB = 1;              // 32-row query blocks per wave
 constexpr int ATT_ROWS = ATT_NW * ATT_RB * 32;  // query rows per block
-constexpr int ATT_CHUNK_PAGES = 128;   // prefix pages per work item (2048 tokens)
+constexpr int ATT_CHUNK_PAGES = 128;   // most prefix pages per work item (2048 tokens); fewer when the
+                                       // grid would otherwise leave the chip idle (attn_plan)
 constexpr int ATT_BS = 16;             // tokens per page
 
 template <typename T> struct AttnT;
@@ -149,7 +150,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const T* __restrict__ k_tree,
     const T* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
-    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max) {
+    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
+    int cp) {
   using AT = AttnT<T>;
   using G = AttnGeom<T, D>;
   constexpr int KPL = AT::KPL, KSTEP = 2 * KPL;
@@ -167,10 +169,10 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
   const int L = ctx_ok ? Lraw : 0;
   const int pages = (L + ATT_BS - 1) / ATT_BS;
-  const int n_chunks = ctx_ok ? max(1, (pages + ATT_CHUNK_PAGES - 1) / ATT_CHUNK_PAGES) : 1;
+  const int n_chunks = ctx_ok ? max(1, (pages + cp - 1) / cp) : 1;
   if (c >= n_chunks) return;
   const bool last = c == n_chunks - 1;
-  const int page0 = c * ATT_CHUNK_PAGES, page1 = min(pages, page0 + ATT_CHUNK_PAGES);
+  const int page0 = c * cp, page1 = min(pages, page0 + cp);
   const int key0 = page0 * ATT_BS, key1 = min(L, page1 * ATT_BS);
 
   // ---- stage page offsets and (last chunk) the ancestor masks; validate what this block reads
@@ -535,7 +537,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
     const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
-    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max) {
+    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
+    int cp) {
   using G = DmaGeom<D>;
   constexpr int NQF = D / 16;         // Q fragments per lane
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
@@ -551,10 +554,10 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
   const int L = ctx_ok ? Lraw : 0;
   const int pages = (L + ATT_BS - 1) / ATT_BS;
-  const int n_chunks = ctx_ok ? max(1, (pages + ATT_CHUNK_PAGES - 1) / ATT_CHUNK_PAGES) : 1;
+  const int n_chunks = ctx_ok ? max(1, (pages + cp - 1) / cp) : 1;
   if (c >= n_chunks) return;
   const bool last = c == n_chunks - 1;
-  const int page0 = c * ATT_CHUNK_PAGES, page1 = min(pages, page0 + ATT_CHUNK_PAGES);
+  const int page0 = c * cp, page1 = min(pages, page0 + cp);
   const int key0 = page0 * ATT_BS, key1 = min(L, page1 * ATT_BS);
 
   const bool bad = attn_meta<D, 2>(meta, ctx_ok, last, page0, page1, block_table + (size_t)b * max_blocks,
@@ -890,14 +893,14 @@ __global__ __launch_bounds__(256) void k_attn_combine(const int32_t* __restrict_
                                                       const float* __restrict__ part_o,
                                                       const float* __restrict__ part_ml, float* __restrict__ out,
                                                       float* __restrict__ lse, int T_, int Hq, int Hkv,
-                                                      int max_blocks, int R, int Rpad, int n_chunks_max) {
+                                                      int max_blocks, int R, int Rpad, int n_chunks_max, int cp) {
   constexpr int TPR = D / 4;                 // threads per row (4 floats each)
   constexpr int RPB = 256 / TPR;             // rows per block
   const int g = blockIdx.y, b = blockIdx.z;
   const int Lraw = ctx_len[b];
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
   const int pages = ctx_ok ? (Lraw + ATT_BS - 1) / ATT_BS : 0;
-  const int n_chunks = ctx_ok ? max(1, (pages + ATT_CHUNK_PAGES - 1) / ATT_CHUNK_PAGES) : 1;
+  const int n_chunks = ctx_ok ? max(1, (pages + cp - 1) / cp) : 1;
   if (n_chunks <= 1) return;
   const int r = blockIdx.x * RPB + threadIdx.x / TPR;
   const int d4 = (threadIdx.x % TPR) * 4;
@@ -935,8 +938,12 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   p.R = d.T * (d.Hq / d.Hkv);
   p.Rpad = (p.R + 31) / 32 * 32;
   p.row_groups = (p.R + ATT_ROWS - 1) / ATT_ROWS;
-  p.chunk_pages = ATT_CHUNK_PAGES;
-  p.n_chunks = std::max(1, (d.max_blocks + ATT_CHUNK_PAGES - 1) / ATT_CHUNK_PAGES);
+  // Few (trajectory, KV head, row group) triples leave most CUs idle unless each prefix is split finer;
+  // with many, finer chunks only add partial results and per-chunk set-up. Chunks stay whole 64-key tiles.
+  const long long triples = (long long)d.B * d.Hkv * p.row_groups;
+  const int cp = triples < 64 ? 32 : ATT_CHUNK_PAGES;
+  p.chunk_pages = cp;
+  p.n_chunks = std::max(1, (d.max_blocks + cp - 1) / cp);
   const size_t rows = (size_t)d.B * d.Hkv * p.n_chunks * p.Rpad;
   p.part_o_bytes = p.n_chunks > 1 ? rows * d.D * sizeof(float) : 0;
   p.part_ml_bytes = p.n_chunks > 1 ? rows * 2 * sizeof(float) : 0;
@@ -953,17 +960,17 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
   if constexpr (sizeof(T) == 2) {
     SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
-              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks);
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages);
   } else {
     SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
-              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks);
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages);
   }
   if (p.n_chunks > 1) {
     constexpr int RPB = 256 / (D / 4);
     dim3 cgrid((p.R + RPB - 1) / RPB, d.Hkv, d.B);
     SR_LAUNCH("sr_attn_combine", (k_attn_combine<D>), cgrid, dim3(256), 0, s, cl, po, pml, out, lse, d.T, d.Hq,
-              d.Hkv, d.max_blocks, p.R, p.Rpad, p.n_chunks);
+              d.Hkv, d.max_blocks, p.R, p.Rpad, p.n_chunks, p.chunk_pages);
   }
   return SR_OK;
 }
