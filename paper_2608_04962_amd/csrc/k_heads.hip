@@ -14,6 +14,7 @@ namespace sr {
 
 // ============================================================================ clip + LayerNorm
 // One block per trajectory: x = h + corr * min(1, c/||corr||) (active rows), n = LN(x).
+constexpr int CLN_MAXE = 32;   // row elements per thread held in registers (d <= 8192)
 template <typename T>
 __global__ __launch_bounds__(256) void k_clip_ln(const T* __restrict__ hidden, const float* __restrict__ corr,
                                                  const uint8_t* __restrict__ active, int d, float clip_norm,
@@ -38,6 +39,46 @@ __global__ __launch_bounds__(256) void k_clip_ln(const T* __restrict__ hidden, c
   const size_t row = (size_t)b * d;
   float scale = 0.f;
   bool act = corr != nullptr && (active == nullptr || active[b] != 0);
+  if (d <= 256 * CLN_MAXE && blockDim.x == 256) {
+    // the row stays in registers: one round trip for the loads, the same sums in the same order
+    float hv[CLN_MAXE], cv[CLN_MAXE];
+#pragma unroll
+    for (int k = 0; k < CLN_MAXE; ++k) {
+      const int i = tid + k * 256;
+      hv[k] = i < d ? Elem<T>::load(hidden, row + i) : 0.f;
+      cv[k] = (act && i < d) ? corr[row + i] : 0.f;
+    }
+    if (act) {
+      float ss = 0.f;
+#pragma unroll
+      for (int k = 0; k < CLN_MAXE; ++k) ss += cv[k] * cv[k];
+      const float nrm = sqrtf(block_sum(ss));
+      scale = nrm > 0.f ? fminf(1.f, clip_norm / nrm) : 0.f;
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < CLN_MAXE; ++k) {
+      const int i = tid + k * 256;
+      hv[k] = hv[k] + (act ? scale * cv[k] : 0.f);
+      if (i < d) {
+        x_out[row + i] = hv[k];
+        s += hv[k];
+      }
+    }
+    const float mean = block_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int k = 0; k < CLN_MAXE; ++k)
+      if (tid + k * 256 < d) { const float v = hv[k] - mean; q += v * v; }
+    const float var = block_sum(q) / (float)d;
+    const float rs = 1.f / sqrtf(var + eps);
+#pragma unroll
+    for (int k = 0; k < CLN_MAXE; ++k) {
+      const int i = tid + k * 256;
+      if (i < d) Elem<T>::store(n_out, row + i, (hv[k] - mean) * rs);
+    }
+    return;
+  }
   if (act) {
     float ss = 0.f;
     for (int i = tid; i < d; i += blockDim.x) { float v = corr[row + i]; ss += v * v; }
@@ -217,6 +258,21 @@ struct EpiLogitsMax {
   }
 };
 
+// wait until at most `ahead` stages of this wave's DMA (LPS transfers each) are outstanding, then meet the
+// block; ahead in [0, MAXA] (the vmcnt immediate must be a constant)
+template <int LPS, int MAXA>
+__device__ __forceinline__ void dma_stage_sync(int ahead) {
+  if constexpr (MAXA > 0) {
+    if (ahead >= MAXA) {
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(MAXA * LPS) : "memory");
+      return;
+    }
+    dma_stage_sync<LPS, MAXA - 1>(ahead);
+  } else {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+}
+
 template <int BM, int BN, int BK, int WGM, int WGN, int STAGES, class Epi>
 __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __restrict__ A,
                                                             const bf16_t* __restrict__ B, int M, int N, int K,
@@ -232,8 +288,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert((A_BLK + B_BLK) % NW == 0 && A_BLK % NW == 0, "DMA blocks must split evenly over the waves");
   static_assert(CPR >= 2 && (CPR & (CPR - 1)) == 0 && BK % 16 == 0, "tile");
-  static_assert(STAGES == 4 || STAGES == 5, "ring of four or five stages");
-  static_assert(3 * LPS <= 63, "three stages of DMA per wave must fit the vmcnt counter");
+  static_assert(STAGES >= 4, "ring of at least four stages");
+  static_assert((STAGES - 2) * LPS <= 63, "the stages in flight must fit the vmcnt counter");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES][A_BYTES + B_BYTES];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -273,12 +329,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   };
   // stage ks has landed for the whole block (the STAGES-3 stages after it may still be in flight) and every
   // wave's LDS reads are done
-  auto sync = [&](int ks) {
-    const int ahead = min(STAGES - 3, nk - 1 - ks);
-    if (ahead >= 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPS) : "memory");
-    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPS) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  };
+  auto sync = [&](int ks) { dma_stage_sync<LPS, STAGES - 3>(min(STAGES - 3, nk - 1 - ks)); };
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -334,13 +385,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 #pragma unroll
   for (int t = 0; t < STAGES - 1; ++t)
     if (t < nk) issue(t);
-  {
-    const int ahead = min(STAGES - 2, nk - 1);   // stages issued after stage 0
-    if (ahead >= 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(3 * LPS) : "memory");
-    else if (ahead == 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPS) : "memory");
-    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPS) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  }
+  dma_stage_sync<LPS, STAGES - 2>(min(STAGES - 2, nk - 1));   // stage 0 landed
   Frags fa_, fb_;
   load(0, fa_);
   for (int ks = 0; ks < nk; ks += 2) {
@@ -619,7 +664,7 @@ static sr_status launch_heads_z_t(const sr_heads_desc& d, const void* hidden, co
     EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
     const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
     dim3 grid(((tn + 7) / 8) * 8 * tm);
-    SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+    SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 8, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
               (const T*)A, d.B, d.H * d.d, d.d, tm, tn, epi);
   } else {
     constexpr int BM = 64, BN = 128, BK = 32;
