@@ -240,8 +240,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
 // memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring: while K-step ks is
 // multiplied, steps up to ks+STAGES-2 are in flight, and the MFMA operand fragments of step ks+1 are read
 // into registers between the two halves of step ks's MFMAs (one barrier per K-step). In LDS a tile row of
-// BK elements is CPR 16-byte chunks; chunk c of row r is stored at position c ^ ((r >> 1) & (CPR - 1)),
-// which keeps the 32x32x16 MFMA operand reads free of bank conflicts. Blocks are mapped so that the
+// BK elements is CPR 16-byte chunks; chunk c of row r is stored at position c ^ gemm_swz<CPR>(r): a
+// 16-byte LDS read serves eight lanes (128 bytes) per cycle, and the eight rows that one such group of
+// the 32x32x16 operand reads touches then fall on distinct 16-byte bank groups. Blocks are mapped so that the
 // M-tiles sharing one N-tile of B run on the same XCD at the same time (B is read from HBM once and hits
 // in that XCD's L2 for the others).
 // Epilogue of the vocabulary GEMM: fp32 logits[m][n] plus, per row, the max over each 64-column group
@@ -273,6 +274,12 @@ __device__ __forceinline__ void dma_stage_sync(int ahead) {
   }
 }
 
+template <int CPR> __device__ __forceinline__ int gemm_swz(int r) {
+  static_assert(CPR == 2 || CPR == 4 || CPR == 8, "rows of 32, 64 or 128 bytes");
+  constexpr int SH = CPR == 8 ? 0 : CPR == 4 ? 1 : 2;   // rows r and r + 8/CPR share bank groups
+  return (r >> SH) & (CPR - 1);
+}
+
 template <int BM, int BN, int BK, int WGM, int WGN, int STAGES, class Epi>
 __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __restrict__ A,
                                                             const bf16_t* __restrict__ B, int M, int N, int K,
@@ -287,7 +294,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert((A_BLK + B_BLK) % NW == 0 && A_BLK % NW == 0, "DMA blocks must split evenly over the waves");
-  static_assert(CPR >= 2 && (CPR & (CPR - 1)) == 0 && BK % 16 == 0, "tile");
+  static_assert(BK == 32 || BK == 64, "tile");
   static_assert(STAGES >= 4, "ring of at least four stages");
   static_assert((STAGES - 2) * LPS <= 63, "the stages in flight must fit the vmcnt counter");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES][A_BYTES + B_BYTES];
@@ -308,14 +315,14 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   for (int j = 0; j < A_BLK / NW; ++j) {
     const int blk = wave + j * NW;
     const int r = blk * RPB + lane / CPR, pos = lane % CPR;
-    const int c = pos ^ ((r >> 1) & (CPR - 1));
+    const int c = pos ^ gemm_swz<CPR>(r);
     srcA[j] = (const unsigned char*)(A + (size_t)min(m0 + r, M - 1) * K) + c * 16;
   }
 #pragma unroll
   for (int j = 0; j < B_BLK / NW; ++j) {
     const int blk = wave + j * NW;
     const int r = blk * RPB + lane / CPR, pos = lane % CPR;
-    const int c = pos ^ ((r >> 1) & (CPR - 1));
+    const int c = pos ^ gemm_swz<CPR>(r);
     srcB[j] = (const unsigned char*)(B + (size_t)min(n0 + r, N - 1) * K) + c * 16;
   }
   // the transfers are untracked by the compiler: every wait on them below is explicit
@@ -349,12 +356,12 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = wm * WTM + i * 32 + fr;
-        f.a[kk][i] = *(const u32x4*)(As + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
+        f.a[kk][i] = *(const u32x4*)(As + r * ROWB + ((c ^ gemm_swz<CPR>(r)) * 16));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = wn * WTN + j * 32 + fr;
-        f.b[kk][j] = *(const u32x4*)(Bs + r * ROWB + ((c ^ ((r >> 1) & (CPR - 1))) * 16));
+        f.b[kk][j] = *(const u32x4*)(Bs + r * ROWB + ((c ^ gemm_swz<CPR>(r)) * 16));
       }
     }
   };
@@ -372,15 +379,16 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   };
   // K-step ks: half of its MFMAs; wait for stage ks+1 and meet the block (every wave is done reading stage
   // ks-1); refill stage ks-1 with step ks+STAGES-1; read step ks+1's fragments; the other half
-  static_assert(BK / 16 == 2, "two MFMA halves per K-step");
   auto step = [&](int ks, const Frags& cur, Frags& nxt) {
-    mma(cur, 0);
+#pragma unroll
+    for (int kk = 0; kk < BK / 32; ++kk) mma(cur, kk);
     if (ks + 1 < nk) {
       sync(ks + 1);
       if (ks + STAGES - 1 < nk) issue(ks + STAGES - 1);
       load(ks + 1, nxt);
     }
-    mma(cur, 1);
+#pragma unroll
+    for (int kk = BK / 32; kk < BK / 16; ++kk) mma(cur, kk);
   };
 #pragma unroll
   for (int t = 0; t < STAGES - 1; ++t)
@@ -395,25 +403,28 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 
   if constexpr (Epi::kTrans) {
     // lane owns row m = .. + l%32; register r of tile j holds column 32*j + 8*(r/4) + 4*(l/32) + r%4
+    static_assert(!Epi::kGroupMax || WTN % 64 == 0, "whole 64-column groups per wave");
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = m0 + wm * WTM + i * 32 + fr;
-      float gm = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+      for (int g = 0; g < (TN + 1) / 2; ++g) {   // 64-column group g of this wave: tiles 2g, 2g+1
+        float gm = -INFINITY;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * fh;
-          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          if (n < N) {
-            if (m < M) epi.store4(m, n, v);
-            gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+        for (int j = 2 * g; j < 2 * g + 2 && j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * fh;
+            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            if (n < N) {
+              if (m < M) epi.store4(m, n, v);
+              gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+            }
           }
+        if constexpr (Epi::kGroupMax) {
+          gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
+          if (fh == 0 && m < M) epi.group_max(m, (n0 + wn * WTN) / 64 + g, gm);
         }
-      if constexpr (Epi::kGroupMax) {
-        static_assert(WTN == 64, "one 64-column group per wave");
-        gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
-        if (fh == 0 && m < M) epi.group_max(m, (n0 + wn * WTN) / 64, gm);
       }
     }
   } else {
@@ -660,11 +671,11 @@ static sr_status launch_heads_z_t(const sr_heads_desc& d, const void* hidden, co
   SR_LAUNCH("sr_clip_ln", (k_clip_ln<T>), dim3(d.B), dim3(256), 0, s, (const T*)hidden, corr, active, d.d,
             d.clip_norm, d.ln_eps, x, (T*)n);
   if constexpr (sizeof(T) == 2) {
-    constexpr int BM = 128, BN = 64, BK = 32;
+    constexpr int BM = 64, BN = 64, BK = 64;
     EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
     const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
     dim3 grid(((tn + 7) / 8) * 8 * tm);
-    SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 8, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
+    SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
               (const T*)A, d.B, d.H * d.d, d.d, tm, tn, epi);
   } else {
     constexpr int BM = 64, BN = 128, BK = 32;
