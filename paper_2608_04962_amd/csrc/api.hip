@@ -277,7 +277,7 @@ static sr_status check_attn_desc(const sr_attn_desc* d) {
 size_t sr_tree_verify_attn_workspace(const sr_attn_desc* d) {
   if (check_attn_desc(d) != SR_OK) return 0;
   const AttnPlan p = attn_plan(*d);
-  return align_up(p.part_o_bytes) + align_up(p.part_ml_bytes);
+  return align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
 }
 
 sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
@@ -292,14 +292,15 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* 
                aligned16(out),
            "q, caches, tree K/V and out must be 16-byte aligned");
   const AttnPlan p = attn_plan(*d);
-  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes);
+  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
   st = check_ws(workspace, workspace_bytes, need);
   if (st != SR_OK) return st;
   char* ws = (char*)workspace;
-  float* po = need ? (float*)ws : nullptr;
-  float* pml = need ? (float*)(ws + align_up(p.part_o_bytes)) : nullptr;
+  float* po = p.part_o_bytes ? (float*)ws : nullptr;
+  float* pml = p.part_ml_bytes ? (float*)(ws + align_up(p.part_o_bytes)) : nullptr;
+  unsigned* work = p.work_bytes ? (unsigned*)(ws + align_up(p.part_o_bytes) + align_up(p.part_ml_bytes)) : nullptr;
   return launch_tree_attn(*d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse, po,
-                          pml, (hipStream_t)stream);
+                          pml, work, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ acceptance

@@ -13,6 +13,7 @@ typedef uint16_t bf16_t;  // bfloat16 storage (bit pattern)
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -44,6 +45,14 @@ __device__ __forceinline__ void lds_dma16_manual(const void* gsrc, unsigned char
   const uint32_t l = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)ldst);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gsrc), "s"(l)
+               : "memory", "m0");
+}
+
+// The same transfer from a uniform base (SGPR pair) plus a 32-bit per-lane byte offset; ldst_u32 is the
+// wave-uniform LDS byte address of the 1 KB destination.
+__device__ __forceinline__ void lds_dma16_sv(uint32_t voff, const void* sbase, uint32_t ldst_u32) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+               "s"(ldst_u32)
                : "memory", "m0");
 }
 

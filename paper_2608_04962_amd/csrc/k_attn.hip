@@ -162,8 +162,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   __shared__ AttnSmem<T, D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-  const int c = blockIdx.x / row_groups, rg = blockIdx.x % row_groups;
-  const int g = blockIdx.y, b = blockIdx.z;
+  const int rg = blockIdx.x % row_groups, bg = blockIdx.x / row_groups;
+  const int g = bg % Hkv, b = bg / Hkv, c = blockIdx.y;
   const int G_ = Hq / Hkv;
   const int Lraw = ctx_len[b];
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
@@ -502,7 +502,7 @@ struct DmaGeom {
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
   static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
-  static constexpr int CPL = (CITEMS + 7 * 64 - 1) / (7 * 64);   // chunks per lane with >= 7 converting waves
+  static constexpr int CG = 4;                          // conversion chunks in flight per lane
   static_assert(BLK % ATT_NW == 0 && CITEMS % 64 == 0, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
@@ -531,24 +531,25 @@ __device__ __forceinline__ void attn_sync(int npd, bool dma_wave, bool ahead) {
   }
 }
 
+// One work item (chunk c of trajectory b, KV head g, row group rg); item = ((c B + b) Hkv + g) row_groups
+// + rg. Whole block; returns with the block's DMA drained. ring: four slots of a K tile then a V tile
+// (bf16 as loaded, fp16 once converted).
 template <int D>
-__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
+__device__ __forceinline__ void attn_item_dma(
+    int item, unsigned char (&ring)[4][2 * DmaGeom<D>::TILE], AttnMeta& meta,
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache, const bf16_t* __restrict__ v_cache,
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
     const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
-    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
-    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
+    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
     int cp) {
   using G = DmaGeom<D>;
   constexpr int NQF = D / 16;         // Q fragments per lane
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
-  // ring slot: K tile, then V tile (bf16 as loaded, fp16 once converted)
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * G::TILE];
-  __shared__ AttnMeta meta;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-  const int c = blockIdx.x / row_groups, rg = blockIdx.x % row_groups;
-  const int g = blockIdx.y, b = blockIdx.z;
+  const int rg = item % row_groups, bg = item / row_groups;
+  const int g = bg % Hkv, b = (bg / Hkv) % B_, c = bg / (Hkv * B_);
   const int G_ = Hq / Hkv;
   const int Lraw = ctx_len[b];
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
@@ -588,7 +589,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   float m_run = -INFINITY, l_run = 0.f;
   // Roles. Without any wave free of query rows, all waves share the DMA and the V conversion. Else
   // the first row-free wave issues all of the DMA (npd = 1), pacing itself on the memory system, and
-  // the other seven waves convert V.
+  // the other waves convert V (a single converting wave would hold the block at the barrier).
   const int n_act = min(ATT_NW, (R - rg * ATT_ROWS + 31) / 32);
   const int n_prod = ATT_NW - n_act;
   const bool wave_active = wave < n_act && !bad;
@@ -638,27 +639,40 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
       lds_dma16_manual(vc_b + vo, slot + G::TILE + blk * 1024);
     }
   };
-  // one producer wave issues the whole tile: for a full prefix tile the four page offsets are read
-  // once and every block's lane offset is a constant; other tiles take the per-lane clamped path
+  // one producer wave issues the whole tile. A full prefix tile is four whole pages: each page's K and V
+  // bases are uniform (scalar registers) and a block's per-lane offset inside its page depends only on
+  // the block's position in the page, so every transfer is a scalar base plus one of BPP lane offsets.
+  // Other tiles take the per-lane clamped path.
   auto issue_prod = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? 0 : key0 + i * ATT_KT;
     if (!tree && t0 + ATT_KT <= key1) {
+      constexpr int BPP = ATT_BS / G::KPB;          // DMA blocks per page
       const int pg = (t0 >> 4) - page0;
-      long long po[ATT_KT / ATT_BS];
-#pragma unroll
-      for (int p = 0; p < ATT_KT / ATT_BS; ++p) po[p] = meta.pgoff[pg + p];
-      // an opaque copy of the lane id keeps the per-block lane offsets from being hoisted out of the
-      // tile loop (32 of them would stay live in registers)
       int ln = lane;
-      asm volatile("" : "+v"(ln));
+      asm volatile("" : "+v"(ln));                  // lane offsets are rebuilt per tile, not kept live
+      uint32_t ko[BPP], vo[BPP];
 #pragma unroll
-      for (int blk = 0; blk < G::BLK; ++blk) {
-        const int kk = blk * G::KPB + ln / G::NCH, pos = ln % G::NCH;
-        const long long row = po[kk >> 4] + (kk & 15) * G::ROWB;
-        lds_dma16_manual(kc_b + row + ((pos ^ (kk & (G::NCH - 1))) * 16), slot + blk * 1024);
-        lds_dma16_manual(vc_b + row + ((pos ^ vswz<G::NCH>(kk)) * 16), slot + G::TILE + blk * 1024);
-        __builtin_amdgcn_sched_barrier(0);        // keep each address next to its transfer
+      for (int j = 0; j < BPP; ++j) {
+        const int kr = j * G::KPB + ln / G::NCH, pos = ln % G::NCH;   // key row in the page, chunk
+        ko[j] = kr * G::ROWB + ((pos ^ (kr & (G::NCH - 1))) * 16);
+        vo[j] = kr * G::ROWB + ((pos ^ vswz<G::NCH>(kr)) * 16);
+      }
+      const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+          (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)slot);
+#pragma unroll
+      for (int p = 0; p < ATT_KT / ATT_BS; ++p) {
+        const long long po0 = meta.pgoff[pg + p];   // same for every lane: made scalar
+        const long long po = (long long)(((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(po0 >> 32)) << 32) |
+                                         __builtin_amdgcn_readfirstlane((uint32_t)po0));
+        const unsigned char* kb = kc_b + po;
+        const unsigned char* vb = vc_b + po;
+#pragma unroll
+        for (int j = 0; j < BPP; ++j) {
+          const int blk = p * BPP + j;
+          lds_dma16_sv(ko[j], kb, lds0 + blk * 1024);
+          lds_dma16_sv(vo[j], vb, lds0 + G::TILE + blk * 1024);
+        }
       }
     } else {
       for (int blk = 0; blk < G::BLK; ++blk) {
@@ -680,20 +694,23 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     const int stride = n_tr * 64;
     int ln = lane;
     asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
-    u32x4 w[G::CPL];
+    for (int base = tr_rank * 64 + ln; base < G::CITEMS; base += G::CG * stride) {
+      u32x4 w[G::CG];
 #pragma unroll
-    for (int k = 0; k < G::CPL; ++k) {
-      const int it = tr_rank * 64 + ln + k * stride;
-      if (it < G::CITEMS) w[k] = *(const u32x4*)(v + it * 16);
-    }
+      for (int k = 0; k < G::CG; ++k) {
+        const int it = base + k * stride;
+        if (it < G::CITEMS) w[k] = *(const u32x4*)(v + it * 16);
+      }
 #pragma unroll
-    for (int k = 0; k < G::CPL; ++k) {
-      const int it = tr_rank * 64 + ln + k * stride;
-      if (it < G::CITEMS) {
-        f16x8 h;
+      for (int k = 0; k < G::CG; ++k) {
+        const int it = base + k * stride;
+        if (it < G::CITEMS) {
+          f16x8 h;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) h[e] = (_Float16)bf2f((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
-        *(f16x8*)(v + it * 16) = h;
+          for (int e = 0; e < 8; ++e)
+            h[e] = (_Float16)bf2f((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
+          *(f16x8*)(v + it * 16) = h;
+        }
       }
     }
   };
@@ -779,11 +796,14 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
         sn[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kq & 1][kt]),
                                                          __builtin_bit_cast(bf16x8, qf[kq]), sn[kt], 0, 0, 0);
 #pragma unroll
-      for (int e = kq * EPQ; e < (kq + 1) * EPQ; ++e) {
+      for (int e = kq * EPQ; e < (kq + 1) * EPQ; e += 2) {
         const int kt = e >> 4, r = e & 15;
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
-        psum += p;
-        pf[kt][r >> 3][r & 7] = (_Float16)p;
+        const _Float16 h0 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
+        const _Float16 h1 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r + 1], scale_log2, -m_use));
+        pf[kt][r >> 3][r & 7] = h0;
+        pf[kt][r >> 3][(r & 7) + 1] = h1;
+        // the row sum takes the fp16 weights the P V product uses, in fp32 (v_dot2_f32_f16)
+        psum = __builtin_amdgcn_fdot2((f16x2){h0, h1}, (f16x2){(_Float16)1.f, (_Float16)1.f}, psum, false);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -887,6 +907,37 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
   }
 }
 
+// Persistent blocks (one per CU) take work items from a counter in item order: every first chunk, then
+// every second chunk, and so on, so the long items start first and the short last chunks fill the tail;
+// items past a trajectory's chunk count return at once. Every wave runs the same iterations (the item
+// is broadcast through LDS), and the loop ends for all once the counter passes n_items.
+template <int D>
+__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache, const bf16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
+    const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
+    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
+    int cp, int n_items, unsigned* __restrict__ work) {
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * DmaGeom<D>::TILE];
+  __shared__ AttnMeta meta;
+  __shared__ int s_item;
+  for (;;) {
+    __syncthreads();                     // every wave is done with the previous item (ring, meta, s_item)
+    if (threadIdx.x == 0) s_item = (int)atomicAdd(work, 1u);
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(s_item);   // uniform: its derived values stay scalar
+    if (item >= n_items) break;
+    attn_item_dma<D>(item, ring, meta, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out,
+                     lse, part_o, part_ml, B_, T_, Hq, Hkv, max_blocks, num_blocks, scale_log2, R, Rpad,
+                     row_groups, n_chunks_max, cp);
+  }
+}
+
+__global__ void k_attn_work_reset(unsigned* __restrict__ work) {
+  if (threadIdx.x == 0) *work = 0u;
+}
+
 // Merge the chunk partials of every (trajectory, KV head) that was split.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_combine(const int32_t* __restrict__ ctx_len,
@@ -947,20 +998,43 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   const size_t rows = (size_t)d.B * d.Hkv * p.n_chunks * p.Rpad;
   p.part_o_bytes = p.n_chunks > 1 ? rows * d.D * sizeof(float) : 0;
   p.part_ml_bytes = p.n_chunks > 1 ? rows * 2 * sizeof(float) : 0;
+  p.work_bytes = d.dtype == SR_BF16 ? sizeof(unsigned) : 0;   // work-item counter of the persistent kernel
   return p;
+}
+
+// compute units of the current device (cached per device)
+static int cu_count() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
 }
 
 template <typename T, int D>
 static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const void* q, const void* kc,
                                const void* vc, const int32_t* bt, const int32_t* cl, const void* kt,
                                const void* vt, const int32_t* par, float* out, float* lse, float* po, float* pml,
-                               hipStream_t s) {
+                               unsigned* work, hipStream_t s) {
   const float scale_log2 = d.scale * kLog2e;
-  dim3 grid(p.n_chunks * p.row_groups, d.Hkv, d.B);
+  // chunk index slowest: consecutive blocks (which the dispatcher deals round-robin to the XCDs) are
+  // different (trajectory, KV head) pairs of one chunk index, so every XCD receives an equal share of the
+  // first chunks (always present) and of the later ones (present only for long contexts); the long
+  // first chunks also start first
+  dim3 grid(d.B * d.Hkv * p.row_groups, p.n_chunks);
   if constexpr (sizeof(T) == 2) {
-    SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
-              (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
-              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages);
+    const long long n_items = (long long)grid.x * grid.y;
+    if (n_items > INT32_MAX / 2) return SR_ERR_INVALID;
+    SR_LAUNCH("sr_attn_reset", k_attn_work_reset, dim3(1), dim3(64), 0, s, work);
+    const int nb = (int)std::min<long long>(n_items, cu_count());
+    SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), dim3(nb), dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
+              (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.B, d.T, d.Hq, d.Hkv,
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages,
+              (int)n_items, work);
   } else {
     SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
@@ -978,10 +1052,10 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
 sr_status launch_tree_attn(const sr_attn_desc& d, const AttnPlan& p, const void* q, const void* k_cache,
                            const void* v_cache, const int32_t* block_table, const int32_t* ctx_len,
                            const void* k_tree, const void* v_tree, const int32_t* parents, float* out,
-                           float* lse, float* part_o, float* part_ml, hipStream_t s) {
+                           float* lse, float* part_o, float* part_ml, unsigned* work, hipStream_t s) {
 #define SR_ATTN_CASE(TT, DD)                                                                                  \
   return launch_attn_t<TT, DD>(d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, \
-                               lse, part_o, part_ml, s)
+                               lse, part_o, part_ml, work, s)
   if (d.dtype == SR_BF16) {
     if (d.D == 128) SR_ATTN_CASE(bf16_t, 128);
     SR_ATTN_CASE(bf16_t, 64);

@@ -30,12 +30,13 @@ struct AttnPlan {
   int chunk_pages;  // prefix pages per work item
   int n_chunks;     // work items per (trajectory, KV head), worst case
   size_t part_o_bytes, part_ml_bytes;
+  size_t work_bytes;  // work-item counter (bf16 path)
 };
 AttnPlan attn_plan(const sr_attn_desc& d);
 sr_status launch_tree_attn(const sr_attn_desc& d, const AttnPlan& p, const void* q, const void* k_cache,
                            const void* v_cache, const int32_t* block_table, const int32_t* ctx_len,
                            const void* k_tree, const void* v_tree, const int32_t* parents, float* out,
-                           float* lse, float* part_o, float* part_ml, hipStream_t s);
+                           float* lse, float* part_o, float* part_ml, unsigned* work, hipStream_t s);
 
 // ---- acceptance (k_accept.hip)
 sr_status launch_tree_accept(const sr_accept_desc& d, const void* target_logits, const float* child_logit,
