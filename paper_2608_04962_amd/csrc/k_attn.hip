@@ -502,11 +502,17 @@ struct DmaGeom {
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
   static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
-  static constexpr int CG = 4;                          // conversion chunks in flight per lane
+  static constexpr int CPL = (CITEMS + 7 * 64 - 1) / (7 * 64);   // chunks per lane with >= 7 converting waves
   static_assert(BLK % ATT_NW == 0 && CITEMS % 64 == 0, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
 };
+
+// max of x over lanes l and l ^ 32 (v_permlane32_swap exchanges the two 32-lane halves without LDS)
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 // chunk-position swizzle of V row k: the eight rows of one transposing read (k mod 4 = 0..3, twice)
 // take four different 64-byte column groups
@@ -688,29 +694,32 @@ __device__ __forceinline__ void attn_item_dma(
     else issue_prod(i, slot);
   };
   // V of a tile, bf16 -> fp16 in place: every converting lane takes whole 16-byte chunks (their positions
-  // do not matter), all of its reads issued first
-  auto convert = [&](unsigned char* v) __attribute__((always_inline)) {
+  // do not matter). The reads (conv_load) are issued early and the converted chunks written later
+  // (conv_store), so the LDS latency overlaps other work.
+  u32x4 cw[G::CPL];
+  auto conv_load = [&](const unsigned char* v) __attribute__((always_inline)) {
     if (tr_rank < 0) return;                    // the DMA wave
-    const int stride = n_tr * 64;
     int ln = lane;
     asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
-    for (int base = tr_rank * 64 + ln; base < G::CITEMS; base += G::CG * stride) {
-      u32x4 w[G::CG];
 #pragma unroll
-      for (int k = 0; k < G::CG; ++k) {
-        const int it = base + k * stride;
-        if (it < G::CITEMS) w[k] = *(const u32x4*)(v + it * 16);
-      }
+    for (int k = 0; k < G::CPL; ++k) {
+      const int it = tr_rank * 64 + ln + k * n_tr * 64;
+      if (it < G::CITEMS) cw[k] = *(const u32x4*)(v + it * 16);
+    }
+  };
+  auto conv_store = [&](unsigned char* v) __attribute__((always_inline)) {
+    if (tr_rank < 0) return;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
 #pragma unroll
-      for (int k = 0; k < G::CG; ++k) {
-        const int it = base + k * stride;
-        if (it < G::CITEMS) {
-          f16x8 h;
+    for (int k = 0; k < G::CPL; ++k) {
+      const int it = tr_rank * 64 + ln + k * n_tr * 64;
+      if (it < G::CITEMS) {
+        f16x8 h;
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            h[e] = (_Float16)bf2f((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
-          *(f16x8*)(v + it * 16) = h;
-        }
+        for (int e = 0; e < 8; ++e)
+          h[e] = (_Float16)bf2f((e & 1) ? (cw[k][e >> 1] >> 16) : (cw[k][e >> 1] & 0xffffu));
+        *(f16x8*)(v + it * 16) = h;
       }
     }
   };
@@ -731,7 +740,9 @@ __device__ __forceinline__ void attn_item_dma(
   };
   // mask, online softmax and O^T += V^T P^T for tile i (scores s); the next tile's scores (K in nks) are
   // computed into sn in the same basic block as this tile's exponentials
-  auto finish = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2]) {
+  float f_muse = 0.f, f_alpha = 1.f;
+  // mask and max of tile i's scores, the new reference max and the rescale of the accumulator
+  auto finish_max = [&](int i, f32x16 (&s)[2]) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
     const bool full = !tree && t0 + ATT_KT <= key1;
@@ -759,7 +770,7 @@ __device__ __forceinline__ void attn_item_dma(
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = max_halves(mx);
     // the reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
     // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled
     const float tmax = mx * scale_log2;
@@ -771,6 +782,13 @@ __device__ __forceinline__ void attn_item_dma(
       for (int dt = 0; dt < NDT; ++dt) o[dt] *= alpha;
     }
     m_run = m_new;
+    f_muse = m_use;
+    f_alpha = alpha;
+  };
+  // exponentials of tile i (scores s), computed in one basic block with the scores of the next tile (K in
+  // nks, into sn), then O^T += V^T P^T with V of tile i (vs)
+  auto finish_rest = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2]) {
+    const float m_use = f_muse, alpha = f_alpha;
     // From here on one basic block, laid out by hand with scheduling fences: each step issues the
     // K fragment reads one step ahead, two score MFMAs of the next tile and 32/NQF of this tile's
     // exponentials (the matrix core works while the vector ALU exponentiates); then the P V MFMAs
@@ -845,9 +863,12 @@ __device__ __forceinline__ void attn_item_dma(
     const int sn_ = (si + 1) & 3, sf = (si + 3) & 3;
     attn_sync<D>(npd, dma_wave, i + 2 < n_tiles);
     if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[sf]);
-    if (i + 1 < n_tiles) convert(ring[sn_] + G::TILE);
+    const bool cv = i + 1 < n_tiles;
+    if (cv) conv_load(ring[sn_] + G::TILE);
+    if (wave_active) finish_max(i, s);
+    if (cv) conv_store(ring[sn_] + G::TILE);
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
-    if (wave_active) finish(i, s, ring[si] + G::TILE, ring[sn_], sn);
+    if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn);
   };
   if (n_tiles > 0) {
     if (dma_wave) {
@@ -856,7 +877,8 @@ __device__ __forceinline__ void attn_item_dma(
     }
     attn_sync<D>(npd, dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
     if (dma_wave && n_tiles > 2) issue(2, ring[2]);
-    convert(ring[0] + G::TILE);
+    conv_load(ring[0] + G::TILE);
+    conv_store(ring[0] + G::TILE);
     if (wave_active) qk(ring[0], sa);
     int si = 0;
     for (int i = 0; i < n_tiles; i += 2) {

@@ -237,9 +237,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
 
 // ============================================================================ bf16 GEMM, direct-to-LDS
 // C[m][n] = sum_k A[m][k] * B[n][k] for bf16 operands (both K-contiguous). Tiles stream from global
-// memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring: while K-step ks is
-// multiplied, steps up to ks+STAGES-2 are in flight, and the MFMA operand fragments of step ks+1 are read
-// into registers between the two halves of step ks's MFMAs (one barrier per K-step). In LDS a tile row of
+// memory straight into LDS (global_load_lds_dwordx4) through a STAGES-deep ring: the MFMA operand
+// fragments of step ks+1 are read into registers between the two halves of step ks's MFMAs (one barrier
+// per K-step), and right after that barrier the slot of step ks (whose fragments are in registers) is
+// refilled with step ks+STAGES, so STAGES-1 steps are in flight. In LDS a tile row of
 // BK elements is CPR 16-byte chunks; chunk c of row r is stored at position c ^ gemm_swz<CPR>(r): a
 // 16-byte LDS read serves eight lanes (128 bytes) per cycle, and the eight rows that one such group of
 // the 32x32x16 operand reads touches then fall on distinct 16-byte bank groups. Blocks are mapped so that the
@@ -295,8 +296,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert((A_BLK + B_BLK) % NW == 0 && A_BLK % NW == 0, "DMA blocks must split evenly over the waves");
   static_assert(BK == 32 || BK == 64, "tile");
-  static_assert(STAGES >= 4, "ring of at least four stages");
-  static_assert((STAGES - 2) * LPS <= 63, "the stages in flight must fit the vmcnt counter");
+  static_assert(STAGES >= 3, "ring of at least three stages");
+  static_assert((STAGES - 1) * LPS <= 63, "the stages in flight must fit the vmcnt counter");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES][A_BYTES + B_BYTES];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -334,9 +335,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 #pragma unroll
     for (int j = 0; j < B_BLK / NW; ++j) lds_dma16_manual(srcB[j] + koff, dst + A_BYTES + (wave + j * NW) * 1024);
   };
-  // stage ks has landed for the whole block (the STAGES-3 stages after it may still be in flight) and every
-  // wave's LDS reads are done
-  auto sync = [&](int ks) { dma_stage_sync<LPS, STAGES - 3>(min(STAGES - 3, nk - 1 - ks)); };
+  // stage ks has landed for the whole block (the stages issued after it, up to ks+STAGES-2, may still be in
+  // flight) and every wave's LDS reads are done
+  auto sync = [&](int ks) { dma_stage_sync<LPS, STAGES - 2>(min(STAGES - 2, nk - 1 - ks)); };
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -378,22 +379,22 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
                                                               __builtin_bit_cast(bf16x8, f.b[kk][j]), acc[i][j], 0, 0, 0);
   };
   // K-step ks: half of its MFMAs; wait for stage ks+1 and meet the block (every wave is done reading stage
-  // ks-1); refill stage ks-1 with step ks+STAGES-1; read step ks+1's fragments; the other half
+  // ks); refill stage ks's slot with step ks+STAGES; read step ks+1's fragments; the other half
   auto step = [&](int ks, const Frags& cur, Frags& nxt) {
 #pragma unroll
     for (int kk = 0; kk < BK / 32; ++kk) mma(cur, kk);
     if (ks + 1 < nk) {
       sync(ks + 1);
-      if (ks + STAGES - 1 < nk) issue(ks + STAGES - 1);
+      if (ks + STAGES < nk) issue(ks + STAGES);
       load(ks + 1, nxt);
     }
 #pragma unroll
     for (int kk = BK / 32; kk < BK / 16; ++kk) mma(cur, kk);
   };
 #pragma unroll
-  for (int t = 0; t < STAGES - 1; ++t)
+  for (int t = 0; t < STAGES; ++t)
     if (t < nk) issue(t);
-  dma_stage_sync<LPS, STAGES - 2>(min(STAGES - 2, nk - 1));   // stage 0 landed
+  dma_stage_sync<LPS, STAGES - 1>(min(STAGES - 1, nk - 1));   // stage 0 landed
   Frags fa_, fb_;
   load(0, fa_);
   for (int ks = 0; ks < nk; ks += 2) {
