@@ -979,22 +979,43 @@ __global__ __launch_bounds__(256) void k_attn_combine(const int32_t* __restrict_
   const int d4 = (threadIdx.x % TPR) * 4;
   if (r >= R) return;
   const size_t base = ((size_t)b * Hkv + g) * n_chunks_max * Rpad + r;
-  float M = -INFINITY;
-  bool nan = false;
-  for (int c = 0; c < n_chunks; ++c) {
-    const float m = part_ml[(base + (size_t)c * Rpad) * 2];
-    const float l = part_ml[(base + (size_t)c * Rpad) * 2 + 1];
-    nan |= isnan(m) || isnan(l);
-    M = fmaxf(M, m);
-  }
-  const float Mu = (M == -INFINITY) ? 0.f : M;
-  float W = 0.f;
+  // chunks in groups of four: every load of a group is in flight at once, then the group is merged into
+  // the running (M, W, acc) (one group, i.e. up to four chunks, is the plain max-then-sum)
+  constexpr int CGRP = 4;
+  float M = -INFINITY, W = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < n_chunks; ++c) {
-    const size_t pr = base + (size_t)c * Rpad;
-    const float w = part_ml[pr * 2 + 1] * exp2f(part_ml[pr * 2] - Mu);
-    W += w;
-    acc += w * *(const f32x4*)(part_o + pr * D + d4);
+  bool nan = false;
+  for (int c0 = 0; c0 < n_chunks; c0 += CGRP) {
+    float2 ml[CGRP];
+    f32x4 po[CGRP];
+#pragma unroll
+    for (int k = 0; k < CGRP; ++k) {
+      const size_t pr = base + (size_t)(c0 + k) * Rpad;
+      if (c0 + k < n_chunks) {
+        ml[k] = *(const float2*)(part_ml + pr * 2);
+        po[k] = *(const f32x4*)(part_o + pr * D + d4);
+      } else {
+        ml[k] = make_float2(-INFINITY, 0.f);
+        po[k] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int k = 0; k < CGRP; ++k) {
+      nan |= isnan(ml[k].x) || isnan(ml[k].y);
+      Mn = fmaxf(Mn, ml[k].x);
+    }
+    const float Mu = (Mn == -INFINITY) ? 0.f : Mn;
+    const float sc = exp2f(M - Mu);           // 0 while nothing is merged yet (M = -inf)
+    W *= sc;
+    acc *= sc;
+#pragma unroll
+    for (int k = 0; k < CGRP; ++k) {
+      const float w = ml[k].y * exp2f(ml[k].x - Mu);
+      W += w;
+      acc += w * po[k];
+    }
+    M = Mn;
   }
   const int G = Hq / Hkv;
   const int t = r / G, h = g * G + r % G;
