@@ -187,6 +187,10 @@ size_t sr_tree_verify_attn_workspace(const sr_attn_desc* desc);
  * Cache slots past ctx_len in a trajectory's last page are never read, nor are
  * block_table entries past its last page. Invalid trajectory (ctx_len out of
  * range, a page id outside [0,num_blocks), bad topology): out and lse are NaN.
+ * Workspace: the partial results of trajectories split into prefix chunks and,
+ * for bf16, the work-item counter of the persistent kernel, which the call
+ * zeroes itself on the stream (no initialisation by the caller). Two calls
+ * that share a workspace must not run concurrently (on one stream they don't).
  */
 sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
                               const void* q, const void* k_cache, const void* v_cache,
