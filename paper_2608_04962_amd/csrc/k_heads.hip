@@ -693,12 +693,27 @@ static sr_status launch_vocab_t(const sr_heads_desc& d, const void* z, const voi
                                 hipStream_t s) {
   const int M = d.B * d.H;
   if constexpr (sizeof(T) == 2) {
-    constexpr int BM = 256, BN = 256, BK = 32;
+    // M = B*H rows: 256-row tiles (8 waves, 128x64 each) when there are enough rows to fill them; at
+    // small batches 128- or 64-row tiles (4 waves) so that the MFMA work does not outgrow the W stream
+    constexpr int BN = 256, BK = 32;
     EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
-    const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
-    dim3 grid(((tn + 7) / 8) * 8 * tm);
-    SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), grid, dim3(512), 0, s,
-              (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+    const int tn = (d.V + BN - 1) / BN;
+    if (M <= 64) {
+      constexpr int BM = 64;
+      const int tm = (M + BM - 1) / BM;
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 1, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
+                dim3(256), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+    } else if (M <= 128) {
+      constexpr int BM = 128;
+      const int tm = (M + BM - 1) / BM;
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 1, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
+                dim3(256), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+    } else {
+      constexpr int BM = 256;
+      const int tm = (M + BM - 1) / BM;
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
+                dim3(512), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+    }
   } else {
     constexpr int BM = 128, BN = 128, BK = 32;
     EpiLogits epi{logits, d.V};

@@ -73,7 +73,9 @@ def test_config0_full():
             np.testing.assert_array_equal(tok[b], otok[b])
 
 
+# B*H rows 15, 96 and 132 take the 64-, 128- and 256-row vocabulary tiles
 @pytest.mark.parametrize("cfg_over", [dict(B=5, d=512, H=3, V=3000, T=16, depth=4),
+                                      dict(B=24, d=512, H=4, V=5000, T=16, depth=4),
                                       dict(B=33, d=256, H=4, V=1000, T=32, depth=5, active_frac=0.5)])
 def test_bf16_scaled(cfg_over):
     cfg = synth.scaled(synth.CONFIGS[2], **cfg_over)
