@@ -33,23 +33,35 @@ constexpr int ACC_NW = 16;
 constexpr int ACC_NT = ACC_NW * 64;
 constexpr int ACC_CH = 512;                  // tokens per chunk = 64 lanes x 8
 constexpr int ACC_MAX_CHUNKS = 512;          // V <= 262144
-constexpr int ACC_GROUP = 4;                 // chunks whose loads a wave issues together
-
+// Row access. A lane's 8 consecutive tokens load as one Raw value (kept packed while in flight: bf16
+// rows take half the registers, so a wave keeps GROUP = 8 chunks' loads in flight instead of 4) and
+// unpack to fp32 when used; ninf() unpacks to eight -inf (lanes past the row).
 template <typename T> struct RowLoad;
 template <> struct RowLoad<bf16_t> {
-  static __device__ __forceinline__ void load8(const bf16_t* p, float* x) {
-    const u32x4 w = *(const u32x4*)p;
+  using Raw = u32x4;
+  static constexpr int GROUP = 8;
+  static __device__ __forceinline__ Raw raw(const bf16_t* p) { return *(const u32x4*)p; }
+  static __device__ __forceinline__ Raw ninf() { return (u32x4){0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u}; }
+  static __device__ __forceinline__ void unpack(const Raw& w, float* x) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) x[e] = bf2f((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
   }
+  static __device__ __forceinline__ void load8(const bf16_t* p, float* x) { unpack(raw(p), x); }
   static __device__ __forceinline__ float load1(const bf16_t* p) { return bf2f(*p); }
 };
 template <> struct RowLoad<float> {
-  static __device__ __forceinline__ void load8(const float* p, float* x) {
-    const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) { x[e] = a[e]; x[e + 4] = b[e]; }
+  struct Raw { f32x4 a, b; };
+  static constexpr int GROUP = 4;
+  static __device__ __forceinline__ Raw raw(const float* p) { return Raw{*(const f32x4*)p, *(const f32x4*)(p + 4)}; }
+  static __device__ __forceinline__ Raw ninf() {
+    const f32x4 n = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    return Raw{n, n};
   }
+  static __device__ __forceinline__ void unpack(const Raw& w, float* x) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { x[e] = w.a[e]; x[e + 4] = w.b[e]; }
+  }
+  static __device__ __forceinline__ void load8(const float* p, float* x) { unpack(raw(p), x); }
   static __device__ __forceinline__ float load1(const float* p) { return *p; }
 };
 
@@ -92,39 +104,41 @@ __device__ __forceinline__ bool nuc_member(const AccSmem& sm, float x, int v) {
   return k > sm.nk_key || (k == sm.nk_key && v <= sm.nk_idcut);
 }
 
-// exp(y - m) with y = x * invtau, as 2^((y - m) log2 e) on the hardware exponential; every step is
-// rounded separately, so the value is identical wherever it is recomputed
+// exp(y - m) with y = x * invtau (m finite), as 2^(x (invtau log2 e) - m log2 e) on the hardware
+// exponential: one fused multiply-add with both factors rounded to fp32 first, the same at every call
+// site, so a token's weight is identical wherever it is recomputed
 __device__ __forceinline__ float tilt(float x, float invtau, float m) {
-  return __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(__fmul_rn(x, invtau), m), kLog2e));
+  return __builtin_amdgcn_exp2f(__builtin_fmaf(x, __fmul_rn(invtau, kLog2e), -__fmul_rn(m, kLog2e)));
 }
 
 template <typename T>
 __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
-  for (int c0 = wave * ACC_GROUP; c0 < nch; c0 += ACC_NW * ACC_GROUP) {
-    float x[ACC_GROUP][8];
+  constexpr int GRP = RowLoad<T>::GROUP;
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    typename RowLoad<T>::Raw w[GRP];
 #pragma unroll
-    for (int gi = 0; gi < ACC_GROUP; ++gi) {
+    for (int gi = 0; gi < GRP; ++gi) {
       const int base = (c0 + gi) * ACC_CH + lane * 8;
-      if (c0 + gi < nch && base < V) {
-        RowLoad<T>::load8(row + base, x[gi]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[gi][e] = -INFINITY;
-      }
+      w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
     }
 #pragma unroll
-    for (int gi = 0; gi < ACC_GROUP; ++gi) {
+    for (int gi = 0; gi < GRP; ++gi) {
       if (c0 + gi >= nch) break;
+      float x[1][8];
+      RowLoad<T>::unpack(w[gi], x[0]);
+      // chunk max of x * invtau: rounding is monotone, so the max of the raw logits times invtau (> 0)
+      // is the max of the products
       float ml = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, __fmul_rn(x[gi][e], invtau));
-      const float m = wave_max_f32(ml);
+      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, x[0][e]);
+      const float m = __fmul_rn(wave_max_f32(ml), invtau);
       float sl = 0.f;                           // at most 512 terms in (0, 1]: fp32 suffices
+      if (m != -INFINITY) {                     // uniform; a -inf token then weighs 2^-inf = 0
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (x[gi][e] != -INFINITY) sl += tilt(x[gi][e], invtau, m);
+        for (int e = 0; e < 8; ++e) sl += tilt(x[0][e], invtau, m);
+      }
       const float s = wave_sum_f32(sl);
       if (lane == 0) { sm.cmax[c0 + gi] = m; sm.csum[c0 + gi] = (double)s; }
     }
@@ -168,27 +182,26 @@ __device__ void nuc_hist(AccSmem& sm, const T* __restrict__ row, int V, float in
   const float M = sm.M;
   for (int i = tid; i < NUC_NB; i += ACC_NT) sm.nh[i] = 0ull;
   __syncthreads();
-  for (int c0 = wave * ACC_GROUP; c0 < nch; c0 += ACC_NW * ACC_GROUP) {
-    float x[ACC_GROUP][8];
+  constexpr int GRP = RowLoad<T>::GROUP;
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    typename RowLoad<T>::Raw w[GRP];
 #pragma unroll
-    for (int gi = 0; gi < ACC_GROUP; ++gi) {
+    for (int gi = 0; gi < GRP; ++gi) {
       const int base = (c0 + gi) * ACC_CH + lane * 8;
-      if (c0 + gi < nch && base < V) {
-        RowLoad<T>::load8(row + base, x[gi]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[gi][e] = -INFINITY;
-      }
+      w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
     }
 #pragma unroll
-    for (int gi = 0; gi < ACC_GROUP; ++gi)
+    for (int gi = 0; gi < GRP; ++gi) {
+      float x[8];
+      RowLoad<T>::unpack(w[gi], x);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float xv = x[gi][e];
+        const float xv = x[e];
         const uint32_t k = acc_key(xv);
         if (xv != -INFINITY && (k & pmask) == prefix)
           atomicAdd(&sm.nh[(k >> sh) & dmask], nuc_fixed(tilt(xv, invtau, M)));
       }
+    }
   }
   __syncthreads();
 }
