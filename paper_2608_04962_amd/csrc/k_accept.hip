@@ -79,6 +79,7 @@ struct AccSmem {
   double csum[ACC_MAX_CHUNKS];
   double cscale[ACC_MAX_CHUNKS];
   int kids[SR_MAX_TREE];
+  double kpt[SR_MAX_TREE];   // unnormalised target weight of each child's token at the current node
   double S;
   int bad;
   int nkid;
@@ -419,10 +420,8 @@ __device__ void draw(AccSmem& sm, const T* __restrict__ row, int V, float invtau
     double a = 0.0;
     if (c < nch) {
       a = sm.csum[c] * sm.cscale[c];
-      for (int k = 0; k < n_excl; ++k) {
-        const int v = sm.tok[sm.kids[k]];
-        if (v / ACC_CH == c) a -= ptilde(sm, row, v, invtau);
-      }
+      for (int k = 0; k < n_excl; ++k)          // the children's weights, kept by the node's slot tests
+        if (sm.tok[sm.kids[k]] / ACC_CH == c) a -= sm.kpt[k];
       a = fmax(a, 0.0);
     }
     adj[i] = a;
@@ -476,15 +475,26 @@ __device__ void draw(AccSmem& sm, const T* __restrict__ row, int V, float invtau
   double w[8];
   double wl = 0.0;
   const int base = cfirst * ACC_CH + lane * 8;
+  unsigned excl = 0;                            // this lane's tokens that are excluded children
+  for (int k = 0; k < n_excl; ++k) {
+    const int v = sm.tok[sm.kids[k]];
+    if (v >= base && v < base + 8) excl |= 1u << (v - base);
+  }
+  float xs[8];
+  if (base < V) {
+    RowLoad<T>::load8(row + base, xs);          // V is a multiple of 8: all 8 tokens are in the row
+  } else {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < 8; ++e) xs[e] = -INFINITY;
+  }
+  const float cm = sm.cmax[cfirst];
+  const double csc = sm.cscale[cfirst];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {               // ptilde of token base + e, from the loaded values
     const int v = base + e;
     double pv = 0.0;
-    if (v < V) {
-      bool ex = false;
-      for (int k = 0; k < n_excl; ++k) ex |= sm.tok[sm.kids[k]] == v;
-      if (!ex) pv = ptilde(sm, row, v, invtau);
-    }
+    if (!((excl >> e) & 1u) && xs[e] != -INFINITY && nuc_member(sm, xs[e], v))
+      pv = (double)tilt(xs[e], invtau, cm) * csc;
     w[e] = pv;
     wl += pv;
   }
@@ -608,6 +618,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
         lg[s] = -INFINITY;
         if (k < m) {
           const double pt = ptilde(sm, row, sm.tok[sm.kids[k]], invtau);
+          sm.kpt[k] = pt;
           r[s] = pt / sm.S;
           lg[s] = (double)sm.cl[sm.kids[k]];
           out_mass_part += pt;
