@@ -75,9 +75,10 @@ struct RfSmem {
   double dd, dc, tvs, sev, pC, pstar;
 };
 
-// exp(y - m) with y = x * invtau, on the hardware exponential
+// exp(y - m) with y = x * invtau (m finite), as 2^(x (invtau log2 e) - m log2 e): one fused
+// multiply-add with both factors rounded to fp32 first, the same wherever it is evaluated
 __device__ __forceinline__ float rf_tilt(float x, float invtau, float m) {
-  return __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(__fmul_rn(x, invtau), m), kLog2e));
+  return __builtin_amdgcn_exp2f(__builtin_fmaf(x, __fmul_rn(invtau, kLog2e), -__fmul_rn(m, kLog2e)));
 }
 
 // One pass over a row: group-max keys, the row max M of x * invtau and Z = sum exp(x * invtau - M).
@@ -110,14 +111,13 @@ __device__ void rf_row_pass(RfSmem& sm, const T* __restrict__ row, int V, float 
       gm = fmaxf(gm, __shfl_xor(gm, 2, 64));
       gm = fmaxf(gm, __shfl_xor(gm, 4, 64));
       if ((lane & 7) == 0 && base < V) sm.gk[c * 8 + (lane >> 3)] = fkey(gm);
-      float ml = -INFINITY;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, __fmul_rn(x[gi][e], invtau));
-      const float m = wave_max_f32(ml);
+      // chunk max of x * invtau from the raw maxima (rounding is monotone and invtau > 0)
+      const float m = __fmul_rn(wave_max_f32(gm), invtau);
       float sl = 0.f;
+      if (m != -INFINITY) {                     // uniform; a -inf token then weighs 2^-inf = 0
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (x[gi][e] != -INFINITY) sl += rf_tilt(x[gi][e], invtau, m);
+        for (int e = 0; e < 8; ++e) sl += rf_tilt(x[gi][e], invtau, m);
+      }
       const float s = wave_sum_f32(sl);
       if (lane == 0) { sm.cmax[c] = m; sm.csum[c] = s; }
     }
