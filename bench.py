@@ -305,9 +305,18 @@ def other_configs(sr, synth, dev, W7=None, A7=None, bias7=None, steps=5, warmup=
         ms = e0.elapsed_time(e1) / steps
         kv = float(L.sum()) * 2 * Hkv * D * 2 + B * T * (Hq + 2 * Hkv) * D * 2 + B * T * Hq * (D + 1) * 4
         am = ams / max(an, 1)
+        # per-kernel durations, one step per kernel name (outside the timed steps)
+        kms = {}
+        for kname in sr.kernel_names():
+            sr.prof_begin(kname)
+            step()
+            kt_ms, kn = sr.prof_end()
+            if kn:
+                kms[kname] = kt_ms
+        torch.cuda.synchronize()
         assert (outs["final_kind"].cpu() != 255).all(), name
         out[name] = {"B": B, "T": T, "ms_per_step": ms, "tree_tokens_per_s": B * T / (ms / 1e3),
-                     "tree_attn_ms": am, "tree_attn_GB/s": kv / (am / 1e3) / 1e9}
+                     "tree_attn_ms": am, "tree_attn_GB/s": kv / (am / 1e3) / 1e9, "kernels_ms": kms}
         log(f"{name}: {ms:.3f} ms/step, {B * T / (ms / 1e3):.4g} tree tokens/s, attention {kv / (am / 1e3) / 1e9:.0f} GB/s")
         del q, kc, vc, kt, vt, tl
         if not seven:
