@@ -577,7 +577,7 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restric
 // m_u children from C_u = top-m_u of head min(depth(u)+1, H), without replacement (Eq. (slotq)).
 // The wave holds C_u across its lanes, so each draw's float64 weights, their sum and the cumulative
 // weights in C_u's order are computed in parallel.
-constexpr int TB_NT = 256;
+constexpr int TB_NT = 1024;           // 16 waves: one node with children per wave at a time
 __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict__ top_id,
                                                      const float* __restrict__ top_val, int H, int M, int T,
                                                      const int32_t* __restrict__ parents,
