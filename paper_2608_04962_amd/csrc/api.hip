@@ -79,7 +79,7 @@ static bool dtype_ok(sr_dtype t) { return t == SR_F32 || t == SR_BF16; }
   } while (0)
 
 struct HeadsLayout {
-  size_t x, n, z, logits, top_id, top_val, gmax, need, total;
+  size_t x, n, z, logits, top_id, top_val, gmax, total;
 };
 static HeadsLayout heads_layout(const sr_heads_desc& d, bool need_z, bool need_logits) {
   HeadsLayout L;
@@ -92,7 +92,6 @@ static HeadsLayout heads_layout(const sr_heads_desc& d, bool need_z, bool need_l
   L.top_id = off; off = align_up(off + B * H * M * 4);
   L.top_val = off; off = align_up(off + B * H * M * 4);
   L.gmax = off; off = align_up(off + group_max_count(d) * 4);
-  L.need = off; off = align_up(off + B * H * 4);
   L.total = off;
   return L;
 }
@@ -177,7 +176,7 @@ sr_status sr_heads_propose(const sr_heads_desc* d, const void* hidden, const flo
   float* gmax = (float*)(ws + L.gmax);
   st = launch_heads(*d, hidden, corr, corr_active, A, bias, W, x, n, zz, lg, gmax, s);
   if (st != SR_OK) return st;
-  return launch_tree_build(*d, lg, gmax, (int32_t*)(ws + L.need), parents, root_token, u_tree, tokens, child_logit,
+  return launch_tree_build(*d, lg, gmax, parents, root_token, u_tree, tokens, child_logit,
                            (int32_t*)(ws + L.top_id), (float*)(ws + L.top_val), s);
 }
 
@@ -223,21 +222,20 @@ sr_status sr_heads_propose_reflex(const sr_heads_desc* d, const sr_reflex_gate_d
   if (st != SR_OK) return st;
   st = launch_vocab(*d, zz, W, lg, gmax, s);
   if (st != SR_OK) return st;
-  return launch_tree_build(*d, lg, gmax, (int32_t*)(ws + L.need), parents, root_token, u_tree, tokens, child_logit,
+  return launch_tree_build(*d, lg, gmax, parents, root_token, u_tree, tokens, child_logit,
                            (int32_t*)(ws + L.top_id), (float*)(ws + L.top_val), s);
 }
 
-static size_t tree_ws_parts(const sr_heads_desc& d, size_t* top, size_t* gm, size_t* need) {
+static size_t tree_ws_parts(const sr_heads_desc& d, size_t* top, size_t* gm) {
   *top = align_up((size_t)d.B * d.H * d.max_children * 4);
   *gm = align_up(group_max_count(d) * 4);
-  *need = align_up((size_t)d.B * d.H * 4);
-  return 2 * *top + *gm + *need;
+  return 2 * *top + *gm;
 }
 
 size_t sr_tree_build_workspace(const sr_heads_desc* d) {
   if (check_heads_desc(d, true) != SR_OK) return 0;
-  size_t a, b, c;
-  return tree_ws_parts(*d, &a, &b, &c);
+  size_t a, b;
+  return tree_ws_parts(*d, &a, &b);
 }
 
 sr_status sr_tree_build(const sr_heads_desc* d, const float* logits, const int32_t* parents,
@@ -246,16 +244,16 @@ sr_status sr_tree_build(const sr_heads_desc* d, const float* logits, const int32
   sr_status st = check_heads_desc(d, true);
   if (st != SR_OK) return st;
   SR_CHECK(logits && parents && root_token && u_tree && tokens && child_logit, "a required pointer is null");
-  size_t top, gm, need;
-  st = check_ws(workspace, workspace_bytes, tree_ws_parts(*d, &top, &gm, &need));
+  size_t top, gm;
+  st = check_ws(workspace, workspace_bytes, tree_ws_parts(*d, &top, &gm));
   if (st != SR_OK) return st;
   char* ws = (char*)workspace;
   float* gmax = (float*)(ws + 2 * top);
   hipStream_t s = (hipStream_t)stream;
   st = launch_group_max(*d, logits, gmax, s);
   if (st != SR_OK) return st;
-  return launch_tree_build(*d, logits, gmax, (int32_t*)(ws + 2 * top + gm), parents, root_token, u_tree, tokens,
-                           child_logit, (int32_t*)ws, (float*)(ws + top), s);
+  return launch_tree_build(*d, logits, gmax, parents, root_token, u_tree, tokens, child_logit, (int32_t*)ws,
+                           (float*)(ws + top), s);
 }
 
 // ------------------------------------------------------------------ attention

@@ -450,20 +450,13 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
 // pass.
 //
 // Exact top-M of a whole row (radix select + id-ordered tie pass). Used directly by the tree build on
-// caller logits, and as the fallback of the grouped selection; ``need`` (optional) restricts the work to
-// rows whose flag is set.
-__global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logits, int V, int M,
-                                                  int32_t* __restrict__ top_id, float* __restrict__ top_val,
-                                                  const int* __restrict__ need) {
-  if (need != nullptr && need[blockIdx.x] == 0) return;
-  __shared__ int hist[TOPM_BINS];
-  __shared__ int scan[TOPM_NT];
-  __shared__ RadixState st;
-  __shared__ int s_n;
-  __shared__ uint32_t ck[SR_MAX_TREE];
-  __shared__ int cid[SR_MAX_TREE];
+// caller logits, and by the grouped selection for a row whose candidates overflow.
+// Exact top-M of one row (whole block): ids and values in (value desc, id asc) order into out_id / out_val.
+// ck / cid hold at least SR_MAX_TREE entries.
+__device__ void topm_row(const float* __restrict__ row, int V, int M, int32_t* __restrict__ out_id,
+                         float* __restrict__ out_val, int* hist, int* scan, RadixState& st, int& s_n, uint32_t* ck,
+                         int* cid) {
   const int tid = threadIdx.x;
-  const float* row = logits + (size_t)blockIdx.x * V;
   if (tid == 0) s_n = 0;
   radix_kth([&](int i) { return fkey(row[i]); }, V, M, hist, scan, st);
   const uint32_t kstar = st.prefix;
@@ -499,9 +492,21 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logi
     const int id = cid[tid];
     int rank = 0;
     for (int j = 0; j < M; ++j) rank += (ck[j] > k) || (ck[j] == k && cid[j] < id);
-    top_id[(size_t)blockIdx.x * M + rank] = id;
-    top_val[(size_t)blockIdx.x * M + rank] = row[id];
+    out_id[rank] = id;
+    out_val[rank] = row[id];
   }
+}
+
+__global__ __launch_bounds__(TOPM_NT) void k_topm(const float* __restrict__ logits, int V, int M,
+                                                  int32_t* __restrict__ top_id, float* __restrict__ top_val) {
+  __shared__ int hist[TOPM_BINS];
+  __shared__ int scan[TOPM_NT];
+  __shared__ RadixState st;
+  __shared__ int s_n;
+  __shared__ uint32_t ck[SR_MAX_TREE];
+  __shared__ int cid[SR_MAX_TREE];
+  const size_t r = blockIdx.x;
+  topm_row(logits + r * V, V, M, top_id + r * M, top_val + r * M, hist, scan, st, s_n, ck, cid);
 }
 
 // Max of every 64-column group of each row (for logits that did not come from the vocabulary GEMM).
@@ -519,13 +524,12 @@ __global__ __launch_bounds__(256) void k_group_max(const float* __restrict__ log
 // Exact top-M of each row using its 64-column group maxima: tau = the M-th largest group max is a lower
 // bound of the M-th largest value (the top M groups each hold an element >= tau), so every top-M element
 // lies in a group whose max is >= tau and is itself >= tau. Only those groups are read. If more than
-// TOPM_CAP elements qualify (heavy ties), the row is flagged for the full selection.
+// TOPM_CAP elements qualify (heavy ties), the same block runs the full selection of the row.
 constexpr int TOPM_MAXG = 4096;     // V <= 262144
 constexpr int TOPM_CAP = 2048;
 __global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restrict__ logits,
                                                           const float* __restrict__ gmax, int V, int ngroups, int M,
-                                                          int32_t* __restrict__ top_id, float* __restrict__ top_val,
-                                                          int* __restrict__ need_full) {
+                                                          int32_t* __restrict__ top_id, float* __restrict__ top_val) {
   __shared__ uint32_t gk[TOPM_MAXG];
   __shared__ int glist[TOPM_MAXG];
   __shared__ int hist[TOPM_BINS];
@@ -558,8 +562,11 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restric
   }
   __syncthreads();
   const int n = s_n;
-  if (tid == 0) need_full[row] = n > TOPM_CAP ? 1 : 0;
-  if (n > TOPM_CAP) return;
+  if (n > TOPM_CAP) {                          // uniform: every thread has read s_n before it is reused
+    __syncthreads();
+    topm_row(lrow, V, M, top_id + (size_t)row * M, top_val + (size_t)row * M, hist, scan, st, s_n, ck, cid);
+    return;
+  }
   for (int t = tid; t < n; t += TOPM_NT) {
     const uint32_t k = ck[t];
     const int id = cid[t];
@@ -746,7 +753,7 @@ sr_status launch_heads(const sr_heads_desc& d, const void* hidden, const float* 
   return launch_vocab(d, z, W, logits, gmax, s);
 }
 
-sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax, int32_t* need_full,
+sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax,
                             const int32_t* parents, const int32_t* root_token, const float* u_tree,
                             int32_t* tokens, float* child_logit, int32_t* top_id, float* top_val, hipStream_t s) {
   const int M = d.max_children;
@@ -755,12 +762,9 @@ sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const f
     const int ng = (d.V + 63) / 64;
     if (gmax != nullptr && ng <= TOPM_MAXG && M <= ng) {
       SR_LAUNCH("sr_topm", k_topm_grouped, dim3(rows), dim3(TOPM_NT), 0, s, logits, gmax, d.V, ng, M, top_id,
-                top_val, need_full);
-      SR_LAUNCH("sr_topm_full", k_topm, dim3(rows), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val,
-                (const int*)need_full);
+                top_val);
     } else {
-      SR_LAUNCH("sr_topm_full", k_topm, dim3(rows), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val,
-                (const int*)nullptr);
+      SR_LAUNCH("sr_topm_full", k_topm, dim3(rows), dim3(TOPM_NT), 0, s, logits, d.V, M, top_id, top_val);
     }
   }
   SR_LAUNCH("sr_tree_build", k_tree_build, dim3(d.B), dim3(TB_NT), 0, s, top_id, top_val, d.H, M, d.T,

@@ -18,7 +18,7 @@ sr_status launch_vocab(const sr_heads_desc& d, const void* z, const void* W, flo
 size_t group_max_count(const sr_heads_desc& d);
 sr_status launch_group_max(const sr_heads_desc& d, const float* logits, float* gmax, hipStream_t s);
 // top-M supports + ordered child lists; gmax may be null (then a full selection per row runs)
-sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax, int32_t* need_full,
+sr_status launch_tree_build(const sr_heads_desc& d, const float* logits, const float* gmax,
                             const int32_t* parents, const int32_t* root_token, const float* u_tree,
                             int32_t* tokens, float* child_logit, int32_t* top_id, float* top_val, hipStream_t s);
 
