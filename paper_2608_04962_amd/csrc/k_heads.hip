@@ -248,8 +248,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm(const T* __restrict__ A
 // in that XCD's L2 for the others).
 // Epilogue of the vocabulary GEMM: fp32 logits[m][n] plus, per row, the max over each 64-column group
 // (the top-M selection scans only groups whose max can reach the M-th largest value). It takes the
-// transposed accumulator layout (a lane owns one row and runs of four consecutive columns), so the
-// logits leave as 16-byte stores and a group max needs one cross-lane exchange. Requires N % 4 == 0.
+// transposed accumulator layout (a lane owns one row and runs of four consecutive columns), so a group
+// max needs one cross-lane exchange; the logits leave through LDS as row-contiguous 16-byte stores.
+// Requires N % 4 == 0.
 struct EpiLogitsMax {
   float* out; float* gmax; int N, ngroups;
   static constexpr bool kGroupMax = true;
@@ -403,11 +404,21 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   }
 
   if constexpr (Epi::kTrans) {
-    // lane owns row m = .. + l%32; register r of tile j holds column 32*j + 8*(r/4) + 4*(l/32) + r%4
+    // lane owns row m = .. + l%32; register r of tile j holds column 32*j + 8*(r/4) + 4*(l/32) + r%4.
+    // Stored straight from registers, each 16-byte store instruction would touch 64 rows (64 cache
+    // lines); instead each wave stages its 32 rows of one tile row through its own part of the ring
+    // (rows padded by 16 bytes: the 16 lanes of a quarter-wave write 16 distinct bank groups) and
+    // stores them back with WTN/4 consecutive lanes per row.
     static_assert(!Epi::kGroupMax || WTN % 64 == 0, "whole 64-column groups per wave");
+    constexpr int RS = WTN * 4 + 16;              // staged row stride in bytes
+    constexpr int LPR = WTN / 4;                  // lanes per staged row on the way out
+    static_assert(64 % LPR == 0, "whole rows per store instruction");
+    static_assert(NW * 32 * RS <= STAGES * (A_BYTES + B_BYTES), "staging fits the ring");
+    __syncthreads();                              // every wave has read its last fragments from the ring
+    unsigned char* stg = &lds[0][0] + wave * 32 * RS;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WTM + i * 32 + fr;
+      const int mb = m0 + wm * WTM + i * 32, m = mb + fr;
 #pragma unroll
       for (int g = 0; g < (TN + 1) / 2; ++g) {   // 64-column group g of this wave: tiles 2g, 2g+1
         float gm = -INFINITY;
@@ -415,17 +426,23 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
         for (int j = 2 * g; j < 2 * g + 2 && j < TN; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * fh;
+            const int c = j * 32 + 8 * q + 4 * fh;
             const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-            if (n < N) {
-              if (m < M) epi.store4(m, n, v);
-              gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-            }
+            *(f32x4*)(stg + fr * RS + c * 4) = v;
+            if (n0 + wn * WTN + c < N) gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
           }
         if constexpr (Epi::kGroupMax) {
           gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
           if (fh == 0 && m < M) epi.group_max(m, (n0 + wn * WTN) / 64 + g, gm);
         }
+      }
+      // this wave's own LDS writes above precede its reads below (one wave, in order)
+#pragma unroll
+      for (int rr = 0; rr < 32; rr += 64 / LPR) {
+        const int row = rr + lane / LPR, c = (lane % LPR) * 4;
+        const f32x4 v = *(const f32x4*)(stg + row * RS + c * 4);
+        const int n = n0 + wn * WTN + c;
+        if (mb + row < M && n < N) epi.store4(mb + row, n, v);
       }
     }
   } else {
