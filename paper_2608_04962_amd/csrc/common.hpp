@@ -111,6 +111,46 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
   const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
   return (a + b) + (c + d);
 }
+// Sums over the wave of N values per lane (N = 4 or 8), reduce-scattered: lane l returns the total of
+// value j = l / (64 / N) (set in j), summed as pairs over lanes l ^ 32 (v_permlane32_swap, which trades
+// the two 32-lane halves of two registers), l ^ 16 and, for N = 8, l ^ 8 (ds_bpermute), then over the low
+// lane bits by DPP. Whole wave active.
+template <int N>
+__device__ __forceinline__ float wave_sum_scatter(const float (&a)[N], int& j) {
+  static_assert(N == 4 || N == 8, "4 or 8 values");
+  const int lane = threadIdx.x & 63;
+  float b[N / 2];
+#pragma unroll
+  for (int k = 0; k < N / 2; ++k) {
+    // lanes 0-31: value k over l, l+32; lanes 32-63: value k + N/2 over l-32, l
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a[k]), __float_as_uint(a[k + N / 2]), false, false);
+    b[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  float v;
+  {
+    const bool hi16 = (lane & 16) != 0;
+    float c[N / 4];
+#pragma unroll
+    for (int k = 0; k < N / 4; ++k) {
+      const float keep = hi16 ? b[k + N / 4] : b[k], send = hi16 ? b[k] : b[k + N / 4];
+      c[k] = keep + __shfl_xor(send, 16, 64);
+    }
+    if constexpr (N == 4) {
+      v = c[0];
+    } else {
+      const bool hi8 = (lane & 8) != 0;
+      const float keep = hi8 ? c[1] : c[0], send = hi8 ? c[0] : c[1];
+      v = keep + __shfl_xor(send, 8, 64);
+    }
+  }
+  // the lanes of one value now differ in their low 6 - log2(N) bits
+  v += dpp_f32<0xB1>(v);                         // quad_perm [1,0,3,2]: lanes i, i ^ 1
+  v += dpp_f32<0x4E>(v);                         // quad_perm [2,3,0,1]: lanes i, i ^ 2
+  v += dpp_f32<0x141>(v);                        // row_half_mirror: quads 0 and 1 of each 8 lanes
+  if constexpr (N == 4) v += dpp_f32<0x140>(v);  // row_mirror: halves of each 16 lanes
+  j = lane / (64 / N);
+  return v;
+}
 template <int CTRL> __device__ __forceinline__ double dpp_f64(double v) {
   const long long u = __double_as_longlong(v);
   const int lo = __builtin_amdgcn_update_dpp((int)u, (int)u, CTRL, 0xf, 0xf, false);

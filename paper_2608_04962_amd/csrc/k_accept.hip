@@ -124,25 +124,36 @@ __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float i
       const int base = (c0 + gi) * ACC_CH + lane * 8;
       w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
     }
+    // One reference max for the GRP chunks of this group: their max of x * invtau (rounding is monotone,
+    // so the max of the raw logits times invtau > 0 is the max of the products). Every consumer weighs a
+    // token of chunk c against cmax[c], so a shared reference only has to be stored per chunk; a token
+    // more than ~87 below it (probability < 1e-37) underflows to weight 0.
+    float ml = -INFINITY;
 #pragma unroll
     for (int gi = 0; gi < GRP; ++gi) {
-      if (c0 + gi >= nch) break;
-      float x[1][8];
-      RowLoad<T>::unpack(w[gi], x[0]);
-      // chunk max of x * invtau: rounding is monotone, so the max of the raw logits times invtau (> 0)
-      // is the max of the products
-      float ml = -INFINITY;
+      float x[8];
+      RowLoad<T>::unpack(w[gi], x);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, x[0][e]);
-      const float m = __fmul_rn(wave_max_f32(ml), invtau);
-      float sl = 0.f;                           // at most 512 terms in (0, 1]: fp32 suffices
-      if (m != -INFINITY) {                     // uniform; a -inf token then weighs 2^-inf = 0
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sl += tilt(x[0][e], invtau, m);
-      }
-      const float s = wave_sum_f32(sl);
-      if (lane == 0) { sm.cmax[c0 + gi] = m; sm.csum[c0 + gi] = (double)s; }
+      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, x[e]);
     }
+    const float m = __fmul_rn(wave_max_f32(ml), invtau);
+    float a[GRP];                               // this lane's part of each chunk sum: 8 terms in (0, 1]
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) a[gi] = 0.f;
+    if (m != -INFINITY) {                       // uniform; a -inf token then weighs 2^-inf = 0
+#pragma unroll
+      for (int gi = 0; gi < GRP; ++gi) {
+        float x[8];
+        RowLoad<T>::unpack(w[gi], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[gi] += tilt(x[e], invtau, m);
+      }
+    }
+    // the GRP chunk sums over the wave at once: each exchange halves the values a lane holds, then the
+    // lanes that share a chunk finish with a plain butterfly; chunk j's total lands in lanes 64/GRP j ..
+    int j;
+    const float s = wave_sum_scatter<GRP>(a, j);
+    if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) { sm.cmax[c0 + j] = m; sm.csum[c0 + j] = (double)s; }
   }
   __syncthreads();
   if (wave == 0) {
