@@ -394,23 +394,37 @@ __device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float inv
   __syncthreads();
 }
 
-// chunk sums restricted to the nucleus (for the terminal draws), relative to the chunk maxima
+// chunk sums restricted to the nucleus (for the terminal draws), relative to the chunks' reference
+// maxima; the same chunk groups and exchanges as row_stats
 template <typename T>
 __device__ void nuc_masked_sums(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
-  for (int c = wave; c < nch; c += ACC_NW) {
-    const int base = c * ACC_CH + lane * 8;
-    float sl = 0.f;
-    if (base < V) {
-      float x[8];
-      RowLoad<T>::load8(row + base, x);
+  constexpr int GRP = RowLoad<T>::GROUP;
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    typename RowLoad<T>::Raw w[GRP];
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (x[e] != -INFINITY && nuc_member(sm, x[e], base + e)) sl += tilt(x[e], invtau, sm.cmax[c]);
+    for (int gi = 0; gi < GRP; ++gi) {
+      const int base = (c0 + gi) * ACC_CH + lane * 8;
+      w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
     }
-    const float s = wave_sum_f32(sl);
-    if (lane == 0) sm.csum[c] = (double)s;
+    float a[GRP];
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) {
+      a[gi] = 0.f;
+      if (c0 + gi < nch) {                      // uniform
+        const int base = (c0 + gi) * ACC_CH + lane * 8;
+        const float m = sm.cmax[c0 + gi];
+        float x[8];
+        RowLoad<T>::unpack(w[gi], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (x[e] != -INFINITY && nuc_member(sm, x[e], base + e)) a[gi] += tilt(x[e], invtau, m);
+      }
+    }
+    int j;
+    const float s = wave_sum_scatter<GRP>(a, j);
+    if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) sm.csum[c0 + j] = (double)s;
   }
   __syncthreads();
 }
