@@ -59,8 +59,8 @@ struct RfSmem {
   int cid[RF_CAP];
   int hist[TOPM_BINS];
   int scan[RF_NT];
-  float cmax[RF_MAXCH];
-  float csum[RF_MAXCH];
+  float cmax[RF_MAXCH / RF_GROUP];   // per group of RF_GROUP chunks: reference max and sum
+  float csum[RF_MAXCH / RF_GROUP];
   RadixState st;
   int s_ng, s_n;
   int top_p[RF_MAXS], top_q[RF_MAXS];
@@ -99,36 +99,42 @@ __device__ void rf_row_pass(RfSmem& sm, const T* __restrict__ row, int V, float 
         for (int e = 0; e < 8; ++e) x[gi][e] = -INFINITY;
       }
     }
+    // 64-token group maxima (lanes 8j .. 8j+7 of a chunk, by DPP), then one reference max and one sum
+    // for the whole group of chunks: only the row's max and sum are kept
+    float ml = -INFINITY;
 #pragma unroll
     for (int gi = 0; gi < RF_GROUP; ++gi) {
       const int c = c0 + gi;
-      if (c >= nch) break;
       const int base = c * RF_CH + lane * 8;
       float gm = x[gi][0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) gm = fmaxf(gm, x[gi][e]);
-      gm = fmaxf(gm, __shfl_xor(gm, 1, 64));
-      gm = fmaxf(gm, __shfl_xor(gm, 2, 64));
-      gm = fmaxf(gm, __shfl_xor(gm, 4, 64));
-      if ((lane & 7) == 0 && base < V) sm.gk[c * 8 + (lane >> 3)] = fkey(gm);
-      // chunk max of x * invtau from the raw maxima (rounding is monotone and invtau > 0)
-      const float m = __fmul_rn(wave_max_f32(gm), invtau);
-      float sl = 0.f;
-      if (m != -INFINITY) {                     // uniform; a -inf token then weighs 2^-inf = 0
+      gm = fmaxf(gm, dpp_f32<0xB1>(gm));        // lanes i, i ^ 1
+      gm = fmaxf(gm, dpp_f32<0x4E>(gm));        // lanes i, i ^ 2
+      gm = fmaxf(gm, dpp_f32<0x141>(gm));       // quads 0 and 1 of each 8 lanes
+      if (c < nch && (lane & 7) == 0 && base < V) sm.gk[c * 8 + (lane >> 3)] = fkey(gm);
+      ml = fmaxf(ml, gm);
+    }
+    // max of x * invtau from the raw maxima (rounding is monotone and invtau > 0)
+    const float m = __fmul_rn(wave_max_f32(ml), invtau);
+    float sl = 0.f;                             // at most 32 terms per lane in (0, 1]
+    if (m != -INFINITY) {                       // uniform; a -inf token then weighs 2^-inf = 0
+#pragma unroll
+      for (int gi = 0; gi < RF_GROUP; ++gi)
 #pragma unroll
         for (int e = 0; e < 8; ++e) sl += rf_tilt(x[gi][e], invtau, m);
-      }
-      const float s = wave_sum_f32(sl);
-      if (lane == 0) { sm.cmax[c] = m; sm.csum[c] = s; }
     }
+    const float s = wave_sum_f32(sl);
+    if (lane == 0) { sm.cmax[c0 / RF_GROUP] = m; sm.csum[c0 / RF_GROUP] = s; }
   }
   __syncthreads();
   if (wave == 0) {
+    const int ng = (nch + RF_GROUP - 1) / RF_GROUP;
     float ml = -INFINITY;
-    for (int c = lane; c < nch; c += 64) ml = fmaxf(ml, sm.cmax[c]);
+    for (int g = lane; g < ng; g += 64) ml = fmaxf(ml, sm.cmax[g]);
     const float M = wave_max_f32(ml);
     double sl = 0.0;
-    for (int c = lane; c < nch; c += 64) sl += (double)sm.csum[c] * exp((double)sm.cmax[c] - (double)M);
+    for (int g = lane; g < ng; g += 64) sl += (double)sm.csum[g] * exp((double)sm.cmax[g] - (double)M);
     const double Z = wave_sum_f64(sl);
     if (lane == 0) { sm.Mrow = M; sm.Zrow = Z; }
   }
