@@ -93,6 +93,7 @@ struct AccSmem {
   double nk_margin;
   unsigned long long nk_above, nk_bin;
   int nk_b;
+  float wred[ACC_NW];        // per-wave partial of a block reduction
 };
 
 __device__ __forceinline__ uint32_t acc_key(float x) {
@@ -332,10 +333,83 @@ __device__ void nuc_tie_cut(AccSmem& sm, const T* __restrict__ row, int V, uint3
   __syncthreads();
 }
 
-// Nucleus cut of the current row (after row_stats): membership fields of sm, sm.S = the nucleus mass and
-// sm.nk_margin. Whole block.
+// Row statistics for the nucleus path, relative to the row max itself: a first pass takes the max, a
+// second computes each token's weight once, for both the chunk sums (cmax[c] = M, cscale[c] = 1) and the
+// first digit of the nucleus histogram (the masses nuc_hist's first pass adds, in the same fixed point).
+// Leaves what row_stats leaves, plus that histogram. Whole block.
+template <typename T>
+__device__ void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  constexpr int GRP = RowLoad<T>::GROUP;
+  for (int i = tid; i < NUC_NB; i += ACC_NT) sm.nh[i] = 0ull;
+  auto load_group = [&](int c0, typename RowLoad<T>::Raw (&w)[GRP]) {
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) {
+      const int base = (c0 + gi) * ACC_CH + lane * 8;
+      w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
+    }
+  };
+  float ml = -INFINITY;
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    typename RowLoad<T>::Raw w[GRP];
+    load_group(c0, w);
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) {
+      float x[8];
+      RowLoad<T>::unpack(w[gi], x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ml = fmaxf(ml, x[e]);
+    }
+  }
+  ml = wave_max_f32(ml);
+  if (lane == 0) sm.wred[wave] = ml;
+  __syncthreads();
+  float mx = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < ACC_NW; ++w) mx = fmaxf(mx, sm.wred[w]);
+  const float M = __fmul_rn(mx, invtau);         // the max of x * invtau (rounding is monotone)
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    typename RowLoad<T>::Raw w[GRP];
+    load_group(c0, w);
+    float a[GRP];
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) a[gi] = 0.f;
+    if (M != -INFINITY) {                        // uniform
+#pragma unroll
+      for (int gi = 0; gi < GRP; ++gi) {
+        float x[8];
+        RowLoad<T>::unpack(w[gi], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float wt = tilt(x[e], invtau, M);
+          a[gi] += wt;
+          if (x[e] != -INFINITY) atomicAdd(&sm.nh[acc_key(x[e]) >> 21], nuc_fixed(wt));
+        }
+      }
+    }
+    int j;
+    const float sc = wave_sum_scatter<GRP>(a, j);
+    if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) { sm.cmax[c0 + j] = M; sm.csum[c0 + j] = (double)sc; }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    double sl = 0.0;
+    for (int c = lane; c < nch; c += 64) {
+      sm.cscale[c] = 1.0;
+      sl += sm.csum[c];
+    }
+    const double S = wave_sum_f64(sl);
+    if (lane == 0) { sm.S = S; sm.M = M; sm.nk_on = 0; }
+  }
+  __syncthreads();
+}
+
+// Nucleus cut of the current row (after row_stats_nuc): membership fields of sm, sm.S = the nucleus mass
+// and sm.nk_margin. Whole block.
 template <typename T>
 __device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float invtau, float top_p) {
+  // the first digit's histogram comes from row_stats_nuc
   const int tid = threadIdx.x, wave = tid >> 6;
   constexpr bool BF = sizeof(T) == 2;
   constexpr int NP = BF ? 2 : 3;
@@ -345,7 +419,7 @@ __device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float inv
   unsigned long long above = 0, target = 0, total = 0;
   for (int pass = 0; pass < NP; ++pass) {
     const uint32_t dmask = (1u << bits[pass]) - 1u;
-    nuc_hist<T>(sm, row, V, invtau, prefix, pmask, shs[pass], dmask);
+    if (pass > 0) nuc_hist<T>(sm, row, V, invtau, prefix, pmask, shs[pass], dmask);
     if (pass == 0) {
       // total mass and the integer target: a token stays iff the mass ranked before it is < top_p * total
       if (wave == 0) {
@@ -566,7 +640,7 @@ __device__ void draw(AccSmem& sm, const T* __restrict__ row, int V, float invtau
   if (lane == 0) { sm.draw_tok = first; sm.draw_margin = margin; }
 }
 
-template <typename T>
+template <typename T, bool NUC>   // NUC: the nucleus cut (top_p < 1) is compiled in
 __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ logits,
                                                         const float* __restrict__ child_logit,
                                                         const int32_t* __restrict__ tokens,
@@ -619,10 +693,12 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   const float Ufin = u_fin[b];
   while (true) {
     const T* row = base + (size_t)u * V;
-    row_stats<T>(sm, row, V, invtau);
-    if (top_p < 1.f) {
+    if constexpr (NUC) {
+      row_stats_nuc<T>(sm, row, V, invtau);
       nucleus<T>(sm, row, V, invtau, top_p);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
+    } else {
+      row_stats<T>(sm, row, V, invtau);
     }
     if (tid == 0) {
       int n = 0;
@@ -692,7 +768,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     const int acc = sm.accepted;
     if (acc < 0) {
       // every child rejected: fallback from the final residual = p outside the children
-      if (top_p < 1.f) nuc_masked_sums<T>(sm, row, V, invtau);
+      if constexpr (NUC) nuc_masked_sums<T>(sm, row, V, invtau);
       if (wave == 0) draw<T>(sm, row, V, invtau, m, Ufin);
       __syncthreads();
       if (tid == 0) {
@@ -711,11 +787,13 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     if (sm.tree.nkids[c] > 0) { u = c; continue; }
     // accepted leaf: bonus token from its own target distribution
     const T* lrow = base + (size_t)c * V;
-    row_stats<T>(sm, lrow, V, invtau);
-    if (top_p < 1.f) {
+    if constexpr (NUC) {
+      row_stats_nuc<T>(sm, lrow, V, invtau);
       nucleus<T>(sm, lrow, V, invtau, top_p);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
       nuc_masked_sums<T>(sm, lrow, V, invtau);
+    } else {
+      row_stats<T>(sm, lrow, V, invtau);
     }
     if (wave == 0) draw<T>(sm, lrow, V, invtau, 0, Ufin);
     __syncthreads();
@@ -735,14 +813,27 @@ sr_status launch_tree_accept(const sr_accept_desc& d, const void* target_logits,
                              const float* u_fin, int32_t* acc_nodes, int32_t* out_tokens, int32_t* out_len,
                              uint8_t* final_kind, float* min_margin, hipStream_t s) {
   const float invtau = 1.0f / d.temperature;
+  const bool nuc = d.top_p < 1.f;
   if (d.logit_dtype == SR_BF16) {
-    SR_LAUNCH("sr_tree_accept", k_tree_accept<bf16_t>, dim3(d.B), dim3(ACC_NT), 0, s,
-              (const bf16_t*)target_logits, child_logit, tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth,
-              invtau, d.top_p, acc_nodes, out_tokens, out_len, final_kind, min_margin);
+    const bf16_t* lg = (const bf16_t*)target_logits;
+    if (nuc)
+      SR_LAUNCH("sr_tree_accept", (k_tree_accept<bf16_t, true>), dim3(d.B), dim3(ACC_NT), 0, s, lg, child_logit,
+                tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth, invtau, d.top_p, acc_nodes, out_tokens,
+                out_len, final_kind, min_margin);
+    else
+      SR_LAUNCH("sr_tree_accept", (k_tree_accept<bf16_t, false>), dim3(d.B), dim3(ACC_NT), 0, s, lg, child_logit,
+                tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth, invtau, d.top_p, acc_nodes, out_tokens,
+                out_len, final_kind, min_margin);
   } else {
-    SR_LAUNCH("sr_tree_accept", k_tree_accept<float>, dim3(d.B), dim3(ACC_NT), 0, s,
-              (const float*)target_logits, child_logit, tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth,
-              invtau, d.top_p, acc_nodes, out_tokens, out_len, final_kind, min_margin);
+    const float* lg = (const float*)target_logits;
+    if (nuc)
+      SR_LAUNCH("sr_tree_accept", (k_tree_accept<float, true>), dim3(d.B), dim3(ACC_NT), 0, s, lg, child_logit,
+                tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth, invtau, d.top_p, acc_nodes, out_tokens,
+                out_len, final_kind, min_margin);
+    else
+      SR_LAUNCH("sr_tree_accept", (k_tree_accept<float, false>), dim3(d.B), dim3(ACC_NT), 0, s, lg, child_logit,
+                tokens, parents, u_acc, u_fin, d.T, d.V, d.max_depth, invtau, d.top_p, acc_nodes, out_tokens,
+                out_len, final_kind, min_margin);
   }
   return SR_OK;
 }
