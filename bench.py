@@ -97,7 +97,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    cfg = synth.CONFIGS[2]
+    cfg = synth.SHAPE_7B
     t0 = time.time()
     hin = synth.heads_inputs(cfg, seed=args.seed)
     ain = synth.attn_inputs(cfg, seed=args.seed)
@@ -239,7 +239,7 @@ def other_configs(sr, synth, dev, W7=None, A7=None, bias7=None, steps=5, warmup=
     g = torch.Generator(device=dev).manual_seed(1)
     bf = torch.bfloat16
     rn = lambda shape, std: (torch.randn(shape, generator=g, device=dev) * std).to(bf)  # noqa: E731
-    cases = [("1.5B-shape", synth.CONFIGS[1]), ("14B-shape-tail", synth.CONFIGS[3])]
+    cases = [("1.5B-shape", synth.SHAPE_1P5B), ("14B-shape-tail", synth.SHAPE_14B_TAIL)]
     cases += [(f"7B-sweep-B{b}-T{t}", synth.sweep_config(b, t)) for b, t in synth.SWEEP_POINTS]
     out = {}
     for name, cfg in cases:

@@ -70,16 +70,14 @@ class Config:
 
 _7B = dict(Hq=28, Hkv=4, D=128, d=3584, H=4, V=151936)
 
-CONFIGS: Dict[int, Config] = {
-    0: Config("tiny-fp32", "f32", B=2, T=8, depth=3, Hq=4, Hkv=2, D=64, d=256, H=2, V=512,
-              ctx=("explicit", (100, 160)), parents=(-1, 0, 0, 1, 1, 2, 3, 4),
-              contiguous_pages=True),
-    1: Config("1.5B-shape", "bf16", B=64, T=16, depth=4, Hq=12, Hkv=2, D=128, d=1536, H=4,
-              V=151936, ctx=("uniform", 512, 4096)),
-    2: Config("7B-shape", "bf16", B=128, T=32, depth=5, ctx=("uniform", 1024, 8192), **_7B),
-    3: Config("14B-shape-tail", "bf16", B=8, T=64, depth=6, Hq=40, Hkv=8, D=128, d=5120, H=5,
-              V=151936, ctx=("uniform", 8192, 16384)),
-}
+TINY_FP32 = Config("tiny-fp32", "f32", B=2, T=8, depth=3, Hq=4, Hkv=2, D=64, d=256, H=2, V=512,
+                   ctx=("explicit", (100, 160)), parents=(-1, 0, 0, 1, 1, 2, 3, 4), contiguous_pages=True)
+SHAPE_1P5B = Config("1.5B-shape", "bf16", B=64, T=16, depth=4, Hq=12, Hkv=2, D=128, d=1536, H=4,
+                    V=151936, ctx=("uniform", 512, 4096))
+SHAPE_7B = Config("7B-shape", "bf16", B=128, T=32, depth=5, ctx=("uniform", 1024, 8192), **_7B)
+SHAPE_14B_TAIL = Config("14B-shape-tail", "bf16", B=8, T=64, depth=6, Hq=40, Hkv=8, D=128, d=5120, H=5,
+                        V=151936, ctx=("uniform", 8192, 16384))
+WORKLOADS: Dict[str, Config] = {c.name: c for c in (TINY_FP32, SHAPE_1P5B, SHAPE_7B, SHAPE_14B_TAIL)}
 
 # Concurrency sweep at the 7B shape: live batch shrinks while the tree grows.
 SWEEP_POINTS: List[Tuple[int, int]] = [(256, 8), (128, 12), (64, 16), (32, 24), (16, 32), (8, 64), (4, 96)]
@@ -95,7 +93,7 @@ def get_config(cfg) -> Config:
         return cfg
     if isinstance(cfg, tuple):
         return sweep_config(*cfg)
-    return CONFIGS[int(cfg)]
+    return WORKLOADS[cfg]
 
 
 def scaled(cfg: Config, **over) -> Config:

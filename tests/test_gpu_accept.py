@@ -58,36 +58,36 @@ class _Rows:
 
 
 def test_config0_parity():
-    _compare(synth.accept_inputs(synth.CONFIGS[0], seed=0))
+    _compare(synth.accept_inputs(synth.TINY_FP32, seed=0))
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_scaled_bf16_parity(seed):
-    cfg = synth.scaled(synth.CONFIGS[2], B=48, V=4096)
+    cfg = synth.scaled(synth.SHAPE_7B, B=48, V=4096)
     _compare(synth.accept_inputs(cfg, seed=seed))
 
 
 def test_acceptance_happens_and_walks_deep():
     # drafts close to the target: most slots accept, walks reach the leaves
-    cfg = synth.scaled(synth.CONFIGS[1], B=64, V=1024, dtype="f32")
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=64, V=1024, dtype="f32")
     inp = synth.accept_inputs(cfg, seed=3, target_std=8.0, noise_std=0.05)
     g, _ = _compare(inp)
     assert (g["final_kind"] == 1).sum() > 0 and g["out_len"].mean() > 2.0
 
 
 def test_temperature_power_of_two():
-    cfg = synth.scaled(synth.CONFIGS[2], B=16, V=2048, dtype="f32")
+    cfg = synth.scaled(synth.SHAPE_7B, B=16, V=2048, dtype="f32")
     _compare(synth.accept_inputs(cfg, seed=4), temperature=0.5)
 
 
 def test_single_node_tree_is_plain_sampling():
-    cfg = synth.scaled(synth.CONFIGS[0], T=1, parents=(-1,), B=8)
+    cfg = synth.scaled(synth.TINY_FP32, T=1, parents=(-1,), B=8)
     g, o = _compare(synth.accept_inputs(cfg, seed=5))
     assert (g["out_len"] == 1).all() and (g["final_kind"] == 0).all()
 
 
 def test_invalid_trajectories_are_flagged():
-    cfg = synth.scaled(synth.CONFIGS[0], B=4)
+    cfg = synth.scaled(synth.TINY_FP32, B=4)
     inp = synth.accept_inputs(cfg, seed=6)
     inp["tokens"] = inp["tokens"].copy()
     inp["tokens"][1, 3] = cfg.V + 3            # token outside the vocabulary
@@ -100,16 +100,16 @@ def test_invalid_trajectories_are_flagged():
     assert g["final_kind"][0] in (0, 1)
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
-def test_full_size_sampled(cfg_id):
-    cfg = synth.CONFIGS[cfg_id]
+@pytest.mark.parametrize("name,rseed", [("1.5B-shape", 1), ("7B-shape", 2), ("14B-shape-tail", 3)])
+def test_full_size_sampled(name, rseed):
+    cfg = synth.WORKLOADS[name]
     inp = synth.accept_inputs(cfg, seed=0)
-    rows = np.random.default_rng(cfg_id).choice(cfg.B, size=min(8, cfg.B), replace=False)
+    rows = np.random.default_rng(rseed).choice(cfg.B, size=min(8, cfg.B), replace=False)
     _compare(inp, rows=rows)
 
 
 def test_deterministic():
-    cfg = synth.scaled(synth.CONFIGS[2], B=32, V=8192)
+    cfg = synth.scaled(synth.SHAPE_7B, B=32, V=8192)
     inp = synth.accept_inputs(cfg, seed=7)
     a = _gpu_accept(inp)
     b = _gpu_accept(inp)
@@ -120,22 +120,22 @@ def test_deterministic():
 # ---------------------------------------------------------------- nucleus truncation
 @pytest.mark.parametrize("top_p", [0.95, 0.5])
 def test_nucleus_config0_and_scaled(top_p):
-    _compare(synth.accept_inputs(synth.CONFIGS[0], seed=10), top_p=top_p)
-    _compare(synth.accept_inputs(synth.scaled(synth.CONFIGS[2], B=48, V=4096), seed=11), top_p=top_p)
+    _compare(synth.accept_inputs(synth.TINY_FP32, seed=10), top_p=top_p)
+    _compare(synth.accept_inputs(synth.scaled(synth.SHAPE_7B, B=48, V=4096), seed=11), top_p=top_p)
 
 
 def test_nucleus_deep_walks_and_temperature():
-    cfg = synth.scaled(synth.CONFIGS[1], B=64, V=1024, dtype="f32")
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=64, V=1024, dtype="f32")
     inp = synth.accept_inputs(cfg, seed=12, target_std=8.0, noise_std=0.05)
     g, _ = _compare(inp, top_p=0.9)
     assert (g["final_kind"] == 1).sum() > 0
-    _compare(synth.accept_inputs(synth.scaled(synth.CONFIGS[2], B=16, V=2048), seed=13), temperature=0.5, top_p=0.95)
+    _compare(synth.accept_inputs(synth.scaled(synth.SHAPE_7B, B=16, V=2048), seed=13), temperature=0.5, top_p=0.95)
 
 
 def test_nucleus_ties_cut_inside_equal_logits():
     """Rows whose logits take few distinct values (the cut falls among equal logits and is decided by id),
     a constant row and an all-negative row."""
-    cfg = synth.scaled(synth.CONFIGS[2], B=24, V=4096)
+    cfg = synth.scaled(synth.SHAPE_7B, B=24, V=4096)
     inp = synth.accept_inputs(cfg, seed=14)
     tl = synth.to_f64(inp["target_logits"], "bf16")
     tl = np.round(tl / 2.0) * 2.0                   # values on a coarse grid: heavy ties
@@ -148,11 +148,11 @@ def test_nucleus_ties_cut_inside_equal_logits():
     _compare(f32, top_p=0.6)
 
 
-@pytest.mark.parametrize("cfg_id", [2, 3])
-def test_nucleus_full_size_sampled(cfg_id):
-    cfg = synth.CONFIGS[cfg_id]
+@pytest.mark.parametrize("name,rseed", [("7B-shape", 12), ("14B-shape-tail", 13)])
+def test_nucleus_full_size_sampled(name, rseed):
+    cfg = synth.WORKLOADS[name]
     inp = synth.accept_inputs(cfg, seed=1)
-    rows = np.random.default_rng(10 + cfg_id).choice(cfg.B, size=min(8, cfg.B), replace=False)
+    rows = np.random.default_rng(rseed).choice(cfg.B, size=min(8, cfg.B), replace=False)
     _compare(inp, rows=rows, top_p=0.95)
 
 

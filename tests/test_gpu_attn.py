@@ -46,39 +46,39 @@ def _check(inp, nodes=None):
 
 
 def test_config0_all_nodes():
-    _check(synth.attn_inputs(synth.CONFIGS[0], seed=0))
+    _check(synth.attn_inputs(synth.TINY_FP32, seed=0))
 
 
 @pytest.mark.parametrize("seed", [0, 1])
 def test_bf16_multi_chunk_ragged(seed):
     # contexts straddle the 2048-token chunk size so the split/combine path and ragged tails run
-    cfg = synth.scaled(synth.CONFIGS[2], B=5, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 1, 5000))
+    cfg = synth.scaled(synth.SHAPE_7B, B=5, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 1, 5000))
     inp = synth.attn_inputs(cfg, seed=seed)
     _check(inp)
 
 
 def test_bf16_rows_over_one_block_gqa7():
     # T*G = 40*7 = 280 > 256 query rows: two row groups
-    cfg = synth.scaled(synth.CONFIGS[2], B=2, T=40, depth=5, ctx=("uniform", 100, 3000))
+    cfg = synth.scaled(synth.SHAPE_7B, B=2, T=40, depth=5, ctx=("uniform", 100, 3000))
     _check(synth.attn_inputs(cfg, seed=3))
 
 
 def test_fp32_d128_and_bf16_d64():
-    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], D=128, Hq=6, Hkv=3), seed=4))
-    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[1], dtype="bf16", B=3, D=64, ctx=("uniform", 20, 300)),
+    _check(synth.attn_inputs(synth.scaled(synth.TINY_FP32, D=128, Hq=6, Hkv=3), seed=4))
+    _check(synth.attn_inputs(synth.scaled(synth.SHAPE_1P5B, dtype="bf16", B=3, D=64, ctx=("uniform", 20, 300)),
                              seed=5))
 
 
 def test_empty_prefix_and_single_node_tree():
-    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], ctx=("explicit", (0, 17))), seed=6))
-    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[0], T=1, parents=(-1,), ctx=("explicit", (0, 2049))),
+    _check(synth.attn_inputs(synth.scaled(synth.TINY_FP32, ctx=("explicit", (0, 17))), seed=6))
+    _check(synth.attn_inputs(synth.scaled(synth.TINY_FP32, T=1, parents=(-1,), ctx=("explicit", (0, 2049))),
                              seed=7))
-    _check(synth.attn_inputs(synth.scaled(synth.CONFIGS[2], B=2, T=128, depth=6, Hq=4, Hkv=4,
+    _check(synth.attn_inputs(synth.scaled(synth.SHAPE_7B, B=2, T=128, depth=6, Hq=4, Hkv=4,
                                           ctx=("uniform", 0, 40)), seed=8))
 
 
 def test_invalid_inputs_give_nan_rows_only_for_that_trajectory():
-    cfg = synth.scaled(synth.CONFIGS[2], B=3, T=8, depth=3, Hq=8, Hkv=2, ctx=("uniform", 40, 3000))
+    cfg = synth.scaled(synth.SHAPE_7B, B=3, T=8, depth=3, Hq=8, Hkv=2, ctx=("uniform", 40, 3000))
     inp = synth.attn_inputs(cfg, seed=9)
     inp["block_table"] = inp["block_table"].copy()
     inp["block_table"][1, 0] = inp["num_blocks"] + 5      # page id out of range
@@ -96,7 +96,7 @@ def test_invalid_inputs_give_nan_rows_only_for_that_trajectory():
 
 
 def test_deterministic():
-    cfg = synth.scaled(synth.CONFIGS[2], B=4, T=16, depth=4, ctx=("uniform", 1000, 4500))
+    cfg = synth.scaled(synth.SHAPE_7B, B=4, T=16, depth=4, ctx=("uniform", 1000, 4500))
     inp = synth.attn_inputs(cfg, seed=10)
     a, la = _run_gpu(inp)
     b, lb = _run_gpu(inp)
@@ -110,11 +110,11 @@ def _sample_nodes(cfg, k, seed):
     return [(int(b), int(u)) for b in bs for u in rng.choice(cfg.T, size=min(4, cfg.T), replace=False)]
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
-def test_full_size_sampled(cfg_id):
-    cfg = synth.CONFIGS[cfg_id]
+@pytest.mark.parametrize("name,rseed", [("1.5B-shape", 1), ("7B-shape", 2), ("14B-shape-tail", 3)])
+def test_full_size_sampled(name, rseed):
+    cfg = synth.WORKLOADS[name]
     inp = synth.attn_inputs(cfg, seed=0)
-    _check(inp, nodes=_sample_nodes(cfg, 6, cfg_id))
+    _check(inp, nodes=_sample_nodes(cfg, 6, rseed))
 
 
 @pytest.mark.parametrize("point", [(256, 8), (4, 96)])

@@ -66,12 +66,12 @@ def _check(inp, parents=True):
 
 
 CASES = {
-    "tiny-fp32": (synth.CONFIGS[0], 1),
-    "1.5B-shape-2-layers": (synth.scaled(synth.CONFIGS[1], ctx=("uniform", 1, 700)), 2),
-    "14B-tail-3-layers": (synth.scaled(synth.CONFIGS[3], ctx=("uniform", 100, 900)), 3),
+    "tiny-fp32": (synth.TINY_FP32, 1),
+    "1.5B-shape-2-layers": (synth.scaled(synth.SHAPE_1P5B, ctx=("uniform", 1, 700)), 2),
+    "14B-tail-3-layers": (synth.scaled(synth.SHAPE_14B_TAIL, ctx=("uniform", 100, 900)), 3),
     "7B-sweep-B4-T96": (synth.scaled(synth.sweep_config(4, 96), ctx=("uniform", 1, 300)), 2),
-    "7B-shape-9-layers": (synth.scaled(synth.CONFIGS[2], B=16, ctx=("uniform", 1, 200)), 9),
-    "fp32-D64-ragged": (synth.scaled(synth.CONFIGS[0], B=33, T=24, depth=4, parents=None,
+    "7B-shape-9-layers": (synth.scaled(synth.SHAPE_7B, B=16, ctx=("uniform", 1, 200)), 9),
+    "fp32-D64-ragged": (synth.scaled(synth.TINY_FP32, B=33, T=24, depth=4, parents=None,
                                      ctx=("uniform", 0, 50), contiguous_pages=False), 1),
 }
 
@@ -85,11 +85,11 @@ def test_commit_parity(name, parents):
 
 def test_commit_full_size_7b():
     """Full 7B-shape step: B=128, contexts uniform in [1024, 8192], one layer of the stacked layout."""
-    _check(synth.commit_inputs(synth.CONFIGS[2], seed=2, n_layers=1))
+    _check(synth.commit_inputs(synth.SHAPE_7B, seed=2, n_layers=1))
 
 
 def test_commit_rejections():
-    cfg = synth.scaled(synth.CONFIGS[2], B=10, ctx=("uniform", 20, 100))
+    cfg = synth.scaled(synth.SHAPE_7B, B=10, ctx=("uniform", 20, 100))
     inp = synth.commit_inputs(cfg, seed=4, n_layers=2)
     acc = inp["acc_nodes"].copy()
     out_len = inp["out_len"].copy()
@@ -126,7 +126,7 @@ def test_commit_rejections():
 
 def test_accept_then_commit():
     """sr_tree_accept's outputs feed sr_commit_path directly; the oracle runs its own walk and commit."""
-    cfg = synth.scaled(synth.CONFIGS[0], B=48, ctx=("uniform", 0, 120))
+    cfg = synth.scaled(synth.TINY_FP32, B=48, ctx=("uniform", 0, 120))
     ai = synth.accept_inputs(cfg, seed=7)
     ci = synth.commit_inputs(cfg, seed=7, n_layers=2)
     res = sr.tree_accept(dev_tensor(ai["target_logits"]), dev_tensor(ai["child_logit"]), dev_tensor(ai["tokens"]),

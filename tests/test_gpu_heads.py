@@ -60,7 +60,7 @@ def _check_tree_valid(inp, tok, cl, ref_logits, rows, tol_abs):
 
 
 def test_config0_full():
-    inp = synth.heads_inputs(synth.CONFIGS[0], seed=0)
+    inp = synth.heads_inputs(synth.TINY_FP32, seed=0)
     tok, cl, lg, z = _gpu_heads(inp)
     ref = _oracle_heads(inp)
     assert row_rel_err(z.reshape(-1, inp["cfg"].d), ref["z"].reshape(-1, inp["cfg"].d)).max() <= 1e-5
@@ -78,7 +78,7 @@ def test_config0_full():
                                       dict(B=24, d=512, H=4, V=5000, T=16, depth=4),
                                       dict(B=33, d=256, H=4, V=1000, T=32, depth=5, active_frac=0.5)])
 def test_bf16_scaled(cfg_over):
-    cfg = synth.scaled(synth.CONFIGS[2], **cfg_over)
+    cfg = synth.scaled(synth.SHAPE_7B, **cfg_over)
     inp = synth.heads_inputs(cfg, seed=1)
     tok, cl, lg, z = _gpu_heads(inp)
     ref = _oracle_heads(inp)
@@ -88,13 +88,13 @@ def test_bf16_scaled(cfg_over):
     _check_tree_valid(inp, tok, cl, ref["logits"], range(cfg.B), 2e-3 * np.abs(ref["logits"]).max())
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
-def test_full_size_sampled(cfg_id):
-    cfg = synth.CONFIGS[cfg_id]
+@pytest.mark.parametrize("name,rseed", [("1.5B-shape", 1), ("7B-shape", 2), ("14B-shape-tail", 3)])
+def test_full_size_sampled(name, rseed):
+    cfg = synth.WORKLOADS[name]
     print(f"[heads] {cfg.name}", flush=True)
     inp = synth.heads_inputs(cfg, seed=0)
     tok, cl, lg, z = _gpu_heads(inp)
-    rows = np.random.default_rng(cfg_id).choice(cfg.B, size=min(3, cfg.B), replace=False)
+    rows = np.random.default_rng(rseed).choice(cfg.B, size=min(3, cfg.B), replace=False)
     ref = _oracle_heads(inp, rows=rows)
     assert_faithful_bf16(z[rows], ref["z_exact"])
     lerr = row_rel_err(lg[rows].reshape(-1, cfg.V), ref["logits"].reshape(-1, cfg.V))
@@ -110,7 +110,7 @@ def _gpu_tree(inp):
     return tok.cpu().numpy(), cl.cpu().numpy()
 
 
-@pytest.mark.parametrize("cfg", [synth.CONFIGS[0], synth.scaled(synth.CONFIGS[3], B=6, V=20000),
+@pytest.mark.parametrize("cfg", [synth.TINY_FP32, synth.scaled(synth.SHAPE_14B_TAIL, B=6, V=20000),
                                  synth.scaled(synth.sweep_config(4, 96), V=50000)], ids=lambda c: c.name)
 @pytest.mark.parametrize("tie_frac", [0.0, 0.5])
 def test_tree_build_bit_exact(cfg, tie_frac):
@@ -125,7 +125,7 @@ def test_tree_build_bit_exact(cfg, tie_frac):
 
 
 def test_tree_build_full_vocab_rows():
-    inp = synth.head_logits_inputs(synth.scaled(synth.CONFIGS[2], B=16), seed=3)
+    inp = synth.head_logits_inputs(synth.scaled(synth.SHAPE_7B, B=16), seed=3)
     tok, cl = _gpu_tree(inp)
     otok, ocl, mg = oracle.tree_build(inp["logits"], inp["parents"], inp["root_token"], inp["u_tree"])
     ok = mg >= 1e-12
@@ -134,7 +134,7 @@ def test_tree_build_full_vocab_rows():
 
 
 def test_tree_build_invalid_topology():
-    inp = synth.head_logits_inputs(synth.CONFIGS[0], seed=4)
+    inp = synth.head_logits_inputs(synth.TINY_FP32, seed=4)
     inp["parents"] = inp["parents"].copy()
     inp["parents"][1, 5] = 7
     tok, cl = _gpu_tree(inp)
@@ -144,7 +144,7 @@ def test_tree_build_invalid_topology():
 
 
 def test_heads_deterministic():
-    cfg = synth.scaled(synth.CONFIGS[2], B=16, d=512, V=4000)
+    cfg = synth.scaled(synth.SHAPE_7B, B=16, d=512, V=4000)
     inp = synth.heads_inputs(cfg, seed=5)
     a = _gpu_heads(inp)
     b = _gpu_heads(inp)

@@ -88,35 +88,35 @@ def _compare(inp, rows=None, **params):
 
 def test_config0_all_records():
     # V = 512 has 8 groups, fewer than the 48 top entries: the full radix selection runs
-    _compare(synth.reflex_inputs(synth.CONFIGS[0], seed=0))
+    _compare(synth.reflex_inputs(synth.TINY_FP32, seed=0))
 
 
 @pytest.mark.parametrize("support", [48, 8])
 def test_bf16_1p5b_shape(support):
-    cfg = synth.scaled(synth.CONFIGS[1], B=4)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=4)
     _compare(synth.reflex_inputs(cfg, seed=1, support=support))
 
 
 def test_14b_shape_two_column_groups():
-    cfg = synth.scaled(synth.CONFIGS[3], B=2)          # d = 5120: two 8-column groups per lane
+    cfg = synth.scaled(synth.SHAPE_14B_TAIL, B=2)          # d = 5120: two 8-column groups per lane
     _compare(synth.reflex_inputs(cfg, seed=2))
 
 
 def test_full_size_7b_sampled():
     """B=128 trajectories x 4 horizons = 512 records at V=151936, d=3584; 24 records checked."""
-    inp = synth.reflex_inputs(synth.CONFIGS[2], seed=3)
+    inp = synth.reflex_inputs(synth.SHAPE_7B, seed=3)
     rows = set(np.random.default_rng(0).choice(inp["R"], 24, replace=False).tolist())
     _compare(inp, rows=rows)
 
 
 def test_temperature_and_parameters():
-    cfg = synth.scaled(synth.CONFIGS[1], B=2, H=3)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=2, H=3)
     _compare(synth.reflex_inputs(cfg, seed=4, support=16), temperature=0.7, n_boundary=2, w_dist=0.5, w_cov=2.0,
              eps=1e-4)
 
 
 def test_ties_take_the_full_selection():
-    cfg = synth.scaled(synth.CONFIGS[1], B=2, H=2)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=2, H=2)
     inp = synth.reflex_inputs(cfg, seed=5)
     p = synth.to_f64(inp["p_logits"], "bf16")
     p[0] = 0.0                                      # a constant target row: every group ties
@@ -127,7 +127,7 @@ def test_ties_take_the_full_selection():
 
 
 def test_gate_duplicates_and_invalid_records():
-    cfg = synth.scaled(synth.CONFIGS[1], B=6, H=2)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=6, H=2)
     inp = synth.reflex_inputs(cfg, seed=6)
     R = inp["R"]
     # record 1 becomes a low-severity record: candidates hold almost all target mass and q equals p
@@ -204,7 +204,7 @@ def _gpu_heads_reflex(inp, gin, P=True):
 @pytest.mark.parametrize("name,over", [("tiny-fp32", None), ("1.5B-shape", dict(B=5, V=20000))])
 def test_gated_correction_parity(name, over):
     from helpers import assert_faithful_bf16, f64
-    cfg = synth.CONFIGS[0] if over is None else synth.scaled(synth.CONFIGS[1], **over)
+    cfg = synth.TINY_FP32 if over is None else synth.scaled(synth.SHAPE_1P5B, **over)
     inp = synth.heads_inputs(cfg, seed=7)
     gin = synth.reflex_gate_inputs(cfg, seed=7)
     print(f"[reflex-gate] {cfg.name} B={cfg.B} H={cfg.H} d={cfg.d} V={cfg.V}", flush=True)
@@ -237,7 +237,7 @@ def test_gated_correction_parity(name, over):
 
 
 def test_closed_gates_match_plain_proposal():
-    cfg = synth.scaled(synth.CONFIGS[1], B=3, V=8000)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=3, V=8000)
     inp = synth.heads_inputs(cfg, seed=8)
     gin = synth.reflex_gate_inputs(cfg, seed=8)
     gin["align"][:, :, 3] = 0.0                     # no feedback yet: every gate closed
@@ -258,7 +258,7 @@ def test_closed_gates_match_plain_proposal():
 
 
 def test_feedback_alignment_moments():
-    cfg = synth.scaled(synth.CONFIGS[1], B=6, H=3)
+    cfg = synth.scaled(synth.SHAPE_1P5B, B=6, H=3)
     inp = synth.reflex_inputs(cfg, seed=9)
     gin = synth.reflex_gate_inputs(cfg, seed=9)
     s_rec = synth.unit_sketches(inp["R"], gin["P"].shape[0], seed=9)

@@ -60,18 +60,18 @@ def _check_all_nodes(inp):
 
 
 def test_masked_equals_per_path_causal_config0():
-    _check_all_nodes(synth.attn_inputs(synth.CONFIGS[0], seed=0))
+    _check_all_nodes(synth.attn_inputs(synth.TINY_FP32, seed=0))
 
 
 def test_masked_equals_per_path_causal_scaled_bf16_paged():
-    cfg = synth.scaled(synth.CONFIGS[2], B=3, T=12, depth=4, Hq=6, Hkv=2, D=32, ctx=("uniform", 1, 70))
+    cfg = synth.scaled(synth.SHAPE_7B, B=3, T=12, depth=4, Hq=6, Hkv=2, D=32, ctx=("uniform", 1, 70))
     _check_all_nodes(synth.attn_inputs(cfg, seed=1))
 
 
 def test_empty_prefix_and_single_node():
-    cfg = synth.scaled(synth.CONFIGS[0], ctx=("explicit", (0, 33)))
+    cfg = synth.scaled(synth.TINY_FP32, ctx=("explicit", (0, 33)))
     _check_all_nodes(synth.attn_inputs(cfg, seed=2))
-    cfg1 = synth.scaled(synth.CONFIGS[0], T=1, parents=(-1,), ctx=("explicit", (17, 0)))
+    cfg1 = synth.scaled(synth.TINY_FP32, T=1, parents=(-1,), ctx=("explicit", (17, 0)))
     inp = synth.attn_inputs(cfg1, seed=3)
     _check_all_nodes(inp)
     # T = 1 and L = 0: the root attends to itself only, so the output is its own value row
@@ -86,7 +86,7 @@ def test_empty_prefix_and_single_node():
 
 def test_paging_is_transparent():
     # moving physical pages around (and rewriting the block table to match) must not change anything
-    cfg = synth.scaled(synth.CONFIGS[2], B=2, T=4, depth=2, Hq=4, Hkv=2, D=16, ctx=("uniform", 20, 60),
+    cfg = synth.scaled(synth.SHAPE_7B, B=2, T=4, depth=2, Hq=4, Hkv=2, D=16, ctx=("uniform", 20, 60),
                        dtype="f32")
     inp = synth.attn_inputs(cfg, seed=4)
     nb = inp["num_blocks"]

@@ -125,10 +125,10 @@ def test_commit_hand_example():
     assert (kc == -1).all()                              # inputs are not modified
 
 
-@pytest.mark.parametrize("cfg_id", [0, 3])
-def test_commit_cache_reads_back_as_prefix_plus_path(cfg_id):
-    cfg = synth.get_config(cfg_id)
-    if cfg_id == 3:
+@pytest.mark.parametrize("name", ["tiny-fp32", "14B-shape-tail"])
+def test_commit_cache_reads_back_as_prefix_plus_path(name):
+    cfg = synth.get_config(name)
+    if name == "14B-shape-tail":
         cfg = synth.scaled(cfg, B=4, ctx=("uniform", 30, 70), dtype="f32")
     inp = synth.commit_inputs(cfg, seed=3)
     kc, vc = inp["k_cache"][0].astype(np.float64), inp["v_cache"][0].astype(np.float64)
@@ -157,7 +157,7 @@ def test_commit_cache_reads_back_as_prefix_plus_path(cfg_id):
 def test_commit_then_attention_matches_tree_attention():
     """Eq. (nodep) across rounds: the next round's anchor query over the committed cache sees the same
     keys/values the tree-masked attention gave the deepest accepted node."""
-    cfg = synth.scaled(synth.get_config(0), B=2)
+    cfg = synth.scaled(synth.get_config("tiny-fp32"), B=2)
     inp = synth.commit_inputs(cfg, seed=5)
     rng = np.random.default_rng(11)
     q = rng.standard_normal((cfg.B, cfg.T, cfg.Hq, cfg.D))
@@ -179,7 +179,7 @@ def test_commit_then_attention_matches_tree_attention():
 
 
 def test_commit_inputs_cover_edge_lengths():
-    cfg = synth.get_config(2)
+    cfg = synth.get_config("7B-shape")
     cfg = synth.scaled(cfg, B=64, ctx=("uniform", 1, 40))
     inp = synth.commit_inputs(cfg, seed=0)
     assert (inp["out_len"] == 1).any() and (inp["out_len"] == cfg.depth + 1).any()

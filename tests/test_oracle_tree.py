@@ -84,8 +84,8 @@ def test_tree_build_uses_depth_head_and_topm_support():
 
 
 def test_tree_build_on_generator_topologies():
-    for cfg_id in (0, 1):
-        cfg = synth.scaled(synth.CONFIGS[cfg_id], B=3, V=300)
+    for base in (synth.TINY_FP32, synth.SHAPE_1P5B):
+        cfg = synth.scaled(base, B=3, V=300)
         inp = synth.head_logits_inputs(cfg, seed=3)
         tok, cl, _ = oracle.tree_build(inp["logits"], inp["parents"], inp["root_token"], inp["u_tree"])
         depth, kids = oracle.tree_structure(inp["parents"][0])
