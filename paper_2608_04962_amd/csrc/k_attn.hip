@@ -29,8 +29,8 @@ constexpr int ATT_KT = 64;             // keys per LDS tile
 constexpr int ATT_NW = 8;              // waves per block
 constexpr int ATT_RB = 1;              // 32-row query blocks per wave
 constexpr int ATT_ROWS = ATT_NW * ATT_RB * 32;  // query rows per block
-constexpr int ATT_CHUNK_PAGES = 128;   // most prefix pages per work item (2048 tokens); fewer when the
-                                       // grid would otherwise leave the chip idle (attn_plan)
+constexpr int ATT_CHUNK_PAGES = 192;   // most prefix pages per work item (3072 tokens): with many
+                                       // (trajectory, KV head) pairs; 128 or 32 with fewer (attn_plan)
 constexpr int ATT_BS = 16;             // tokens per page
 
 template <typename T> struct AttnT;
@@ -1035,7 +1035,7 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   // Few (trajectory, KV head, row group) triples leave most CUs idle unless each prefix is split finer;
   // with many, finer chunks only add partial results and per-chunk set-up. Chunks stay whole 64-key tiles.
   const long long triples = (long long)d.B * d.Hkv * p.row_groups;
-  const int cp = triples < 64 ? 32 : ATT_CHUNK_PAGES;
+  const int cp = triples < 64 ? 32 : triples < 512 ? 128 : ATT_CHUNK_PAGES;
   p.chunk_pages = cp;
   p.n_chunks = std::max(1, (d.max_blocks + cp - 1) / cp);
   const size_t rows = (size_t)d.B * d.Hkv * p.n_chunks * p.Rpad;
