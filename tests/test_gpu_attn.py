@@ -57,6 +57,13 @@ def test_bf16_multi_chunk_ragged(seed):
     _check(inp)
 
 
+def test_bf16_long_chunks_all_nodes():
+    # 512 (trajectory, KV head) pairs select 192-page prefix chunks: contexts of 2900-6200 tokens take one
+    # to three chunks, with ragged tails; every node of every trajectory is compared
+    cfg = synth.scaled(synth.SHAPE_7B, B=128, T=2, depth=1, ctx=("uniform", 2900, 6200))
+    _check(synth.attn_inputs(cfg, seed=5))
+
+
 def test_bf16_rows_over_one_block_gqa7():
     # T*G = 40*7 = 280 > 256 query rows: two row groups
     cfg = synth.scaled(synth.SHAPE_7B, B=2, T=40, depth=5, ctx=("uniform", 100, 3000))
