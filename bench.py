@@ -164,12 +164,16 @@ def main():
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]   # per-step spread
     ev0.record()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        marks[i].record()
         step()
+    marks[-1].record()
     ev1.record()
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
+    per_step = np.sort(np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]))
     dom_ms, dom_n = sr.prof_end()
     ms_per_step = total_ms / args.steps
     dom_avg_ms = dom_ms / max(dom_n, 1)
@@ -199,6 +203,8 @@ def main():
                    "global_batch": B, "tree_nodes": T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                      "traffic": measured_traffic(dominant), "kernel": dominant, "avg_ms": dom_avg_ms, "launches": dom_n},
+        "step_ms": {"p50": float(np.percentile(per_step, 50)), "p90": float(np.percentile(per_step, 90)),
+                    "min": float(per_step[0]), "max": float(per_step[-1])},
         "tree_attn": {"GB/s": attn_gbps, "frac_hbm_peak": attn_gbps / HBM_PEAK_GBPS, "ms": attn_ms},
         "kernels_ms": per_kernel,
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
