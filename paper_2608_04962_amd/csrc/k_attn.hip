@@ -547,8 +547,8 @@ __device__ __forceinline__ void attn_item_dma(
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
     const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
-    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
-    int cp) {
+    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
+    int n_chunks_max, int cp) {
   using G = DmaGeom<D>;
   constexpr int NQF = D / 16;         // Q fragments per lane
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
@@ -571,8 +571,9 @@ __device__ __forceinline__ void attn_item_dma(
                                    parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
 
   // ---- this wave's 32 query rows: row r <-> (node t = r / G, head g*G + r % G)
-  const int my_r = rg * ATT_ROWS + wave * 32 + (lane & 31);
-  const bool row_ok = my_r < R;
+  const int rend = min(R, (rg + 1) * group_rows);   // this row group's rows: [rg group_rows, rend)
+  const int my_r = rg * group_rows + wave * 32 + (lane & 31);
+  const bool row_ok = my_r < rend;
   const int my_t = row_ok ? my_r / G_ : 0;
   u32x4 qf[NQF];
   {
@@ -596,7 +597,7 @@ __device__ __forceinline__ void attn_item_dma(
   // Roles. Without any wave free of query rows, all waves share the DMA and the V conversion. Else
   // the first row-free wave issues all of the DMA (npd = 1), pacing itself on the memory system, and
   // the other waves convert V (a single converting wave would hold the block at the barrier).
-  const int n_act = min(ATT_NW, (R - rg * ATT_ROWS + 31) / 32);
+  const int n_act = min(ATT_NW, (rend - rg * group_rows + 31) / 32);
   const int n_prod = ATT_NW - n_act;
   const bool wave_active = wave < n_act && !bad;
   const int npd = n_prod == 0 ? ATT_NW : 1;
@@ -939,8 +940,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
     const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
-    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
-    int cp, int n_items, unsigned* __restrict__ work) {
+    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
+    int n_chunks_max, int cp, int n_items, unsigned* __restrict__ work) {
   __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * DmaGeom<D>::TILE];
   __shared__ AttnMeta meta;
   __shared__ int s_item;
@@ -952,7 +953,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     if (item >= n_items) break;
     attn_item_dma<D>(item, ring, meta, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out,
                      lse, part_o, part_ml, B_, T_, Hq, Hkv, max_blocks, num_blocks, scale_log2, R, Rpad,
-                     row_groups, n_chunks_max, cp);
+                     row_groups, group_rows, n_chunks_max, cp);
   }
 }
 
@@ -1031,7 +1032,14 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   AttnPlan p;
   p.R = d.T * (d.Hq / d.Hkv);
   p.Rpad = (p.R + 31) / 32 * 32;
-  p.row_groups = (p.R + ATT_ROWS - 1) / ATT_ROWS;
+  // bf16: more than one block's rows split evenly into groups of at most 224 rows, so every work item
+  // keeps a wave free of query rows to issue its DMA (fp32: groups of 256)
+  p.group_rows = ATT_ROWS;
+  if (d.dtype == SR_BF16 && p.R > ATT_ROWS) {
+    const int ng = (p.R + (ATT_ROWS - 32) - 1) / (ATT_ROWS - 32);
+    p.group_rows = ((p.R + ng - 1) / ng + 31) / 32 * 32;
+  }
+  p.row_groups = (p.R + p.group_rows - 1) / p.group_rows;
   // Few (trajectory, KV head, row group) triples leave most CUs idle unless each prefix is split finer;
   // with many, finer chunks only add partial results and per-chunk set-up. Chunks stay whole 64-key tiles.
   const long long triples = (long long)d.B * d.Hkv * p.row_groups;
@@ -1076,8 +1084,8 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
     const int nb = (int)std::min<long long>(n_items, cu_count());
     SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), dim3(nb), dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.B, d.T, d.Hq, d.Hkv,
-              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages,
-              (int)n_items, work);
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.group_rows, p.n_chunks,
+              p.chunk_pages, (int)n_items, work);
   } else {
     SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,

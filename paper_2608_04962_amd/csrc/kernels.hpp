@@ -27,6 +27,7 @@ struct AttnPlan {
   int R;            // query rows per (trajectory, KV head) = T * Hq / Hkv
   int Rpad;         // R rounded up to 32
   int row_groups;   // blocks along the rows
+  int group_rows;   // query rows per row group (a multiple of 32, at most 256)
   int chunk_pages;  // prefix pages per work item
   int n_chunks;     // work items per (trajectory, KV head), worst case
   size_t part_o_bytes, part_ml_bytes;
