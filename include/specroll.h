@@ -156,9 +156,11 @@ sr_status sr_tree_build(const sr_heads_desc* desc, const float* logits,
  *   out[b][u][h] = softmax(scale * q . K^T) V,   lse[b][u][h] = logsumexp(scale * q . K^T)
  * which equals ordinary causal attention at u's position of the sequence
  * prefix ++ path(u). Scores and softmax are fp32. For bf16 inputs the
- * probability-weighted sum over V runs on fp16 matrix cores: V entries are
- * converted bf16 -> fp16 (exact for |v| in [2^-14, 65504]; smaller magnitudes
- * lose relative precision, larger ones overflow to inf).
+ * probability-weighted sum over V runs on fp16 matrix cores with V converted
+ * bf16 -> fp16, which is exact for zero and for |v| in [2^-14, 65280]; a work
+ * item (trajectory, KV head, prefix chunk) whose V holds any other value
+ * (larger, smaller, subnormal or non-finite) is recomputed with V in fp32, so
+ * every finite bf16 V gives the fp32-accumulated result.
  */
 typedef struct {
   int32_t B, T;          /* trajectories; tree nodes (1..SR_MAX_TREE)           */
@@ -188,8 +190,9 @@ size_t sr_tree_verify_attn_workspace(const sr_attn_desc* desc);
  * block_table entries past its last page. Invalid trajectory (ctx_len out of
  * range, a page id outside [0,num_blocks), bad topology): out and lse are NaN.
  * Workspace: the partial results of trajectories split into prefix chunks and,
- * for bf16, the work-item counter of the persistent kernel, which the call
- * zeroes itself on the stream (no initialisation by the caller). Two calls
+ * for bf16, the work-item counter of the persistent kernel and the list of work
+ * items to recompute with fp32 V, whose counters the call zeroes itself with a
+ * kernel on the stream (no initialisation by the caller, no memset). Two calls
  * that share a workspace must not run concurrently (on one stream they don't).
  */
 sr_status sr_tree_verify_attn(const sr_attn_desc* desc,

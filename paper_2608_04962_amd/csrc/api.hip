@@ -278,10 +278,9 @@ size_t sr_tree_verify_attn_workspace(const sr_attn_desc* d) {
   return align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
 }
 
-sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
-                              const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
-                              const void* v_tree, const int32_t* parents, float* out, float* lse, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+static sr_status check_attn_args(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
+                                 const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
+                                 const void* v_tree, const int32_t* parents, const float* out) {
   sr_status st = check_attn_desc(d);
   if (st != SR_OK) return st;
   SR_CHECK(q && k_cache && v_cache && block_table && ctx_len && k_tree && v_tree && parents && out,
@@ -289,16 +288,32 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* 
   SR_CHECK(aligned16(q) && aligned16(k_cache) && aligned16(v_cache) && aligned16(k_tree) && aligned16(v_tree) &&
                aligned16(out),
            "q, caches, tree K/V and out must be 16-byte aligned");
-  const AttnPlan p = attn_plan(*d);
-  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
-  st = check_ws(workspace, workspace_bytes, need);
-  if (st != SR_OK) return st;
-  char* ws = (char*)workspace;
+  return SR_OK;
+}
+
+static sr_status run_attn(const sr_attn_desc* d, const AttnPlan& p, const void* q, const void* k_cache,
+                          const void* v_cache, const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
+                          const void* v_tree, const int32_t* parents, float* out, float* lse, char* ws,
+                          void* stream) {
   float* po = p.part_o_bytes ? (float*)ws : nullptr;
   float* pml = p.part_ml_bytes ? (float*)(ws + align_up(p.part_o_bytes)) : nullptr;
   unsigned* work = p.work_bytes ? (unsigned*)(ws + align_up(p.part_o_bytes) + align_up(p.part_ml_bytes)) : nullptr;
   return launch_tree_attn(*d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse, po,
                           pml, work, (hipStream_t)stream);
+}
+
+sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
+                              const void* v_tree, const int32_t* parents, float* out, float* lse, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  sr_status st = check_attn_args(d, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out);
+  if (st != SR_OK) return st;
+  const AttnPlan p = attn_plan(*d);
+  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
+  st = check_ws(workspace, workspace_bytes, need);
+  if (st != SR_OK) return st;
+  return run_attn(d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse,
+                  (char*)workspace, stream);
 }
 
 // ------------------------------------------------------------------ acceptance

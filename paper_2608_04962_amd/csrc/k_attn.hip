@@ -6,16 +6,26 @@
 //
 // Work item = (trajectory b, KV head g, prefix chunk c, row group). The query rows of one
 // work item are the T*G (node, head-in-group) pairs sharing KV head g, so every K/V tile
-// staged in LDS is reused by all of them (GQA sharing). Each wave owns two 32-row blocks of
-// query rows (every K/V fragment read from LDS feeds two MFMAs) and computes transposed scores
+// staged in LDS is reused by all of them (GQA sharing). Scores are computed transposed,
 // S^T = K Q^T on 32x32 MFMA tiles: a lane then holds 16 keys of one query row, so the row max
-// needs one cross-half exchange. P stays in registers and feeds O^T = V^T P^T; V is transposed
-// into LDS when staged. One wave per SIMD leaves room for the accumulators in AGPRs; tile i+1
-// is fetched into registers while tile i is computed from LDS (two LDS stages). bf16 scores use
-// v_mfma_f32_32x32x16_bf16; the probability-weighted V sum uses v_mfma_f32_32x32x16_f16
-// with P and V in fp16 (bf16 P would cost ~3e-3 relative error at 4k-token contexts).
-// The last chunk of a trajectory also processes the T tree keys under the ancestor mask.
-// Several chunks of one (b, g) are merged by log-sum-exp in k_attn_combine.
+// needs one cross-half exchange; P stays in registers and feeds O^T = V^T P^T. The last chunk
+// of a trajectory also processes the T tree keys under the ancestor mask. Several chunks of
+// one (b, g) are merged by log-sum-exp in k_attn_combine.
+//
+// Three kernels share the item decomposition:
+// * k_tree_attn_dma<D> (bf16): one persistent block of eight waves per CU takes items from a
+//   counter. A row group holds at most 224 rows, so at least one wave has no query rows and
+//   issues all K/V transfers straight from HBM into a four-slot LDS ring; every other wave owns
+//   32 query rows and converts a share of each V tile from bf16 to fp16 in place. Scores use
+//   v_mfma_f32_32x32x16_bf16, the probability-weighted V sum v_mfma_f32_32x32x16_f16 with P and
+//   V in fp16 (bf16 P would cost ~3e-3 relative error at 4k-token contexts). fp16 holds a bf16
+//   value exactly only for magnitudes in [2^-14, 65280] (or zero); the converting waves track the
+//   range of every V value they convert, and an item that meets any other value is listed for
+//   k_tree_attn_redo, which recomputes it.
+// * k_tree_attn_redo<D> (bf16): the listed items, one block each, with V widened to fp32 and the
+//   weighted sum on fp32 MFMA (exact for every finite bf16 V).
+// * k_tree_attn<AT, D> (fp32 inputs; and the redo path's item body): one block per item, K/V
+//   staged through registers into a two-slot LDS ring with V transposed, eight waves of 32 rows.
 #include <math.h>
 
 #include <type_traits>
@@ -33,29 +43,33 @@ constexpr int ATT_CHUNK_PAGES = 192;   // most prefix pages per work item (3072 
                                        // (trajectory, KV head) pairs; 128 or 32 with fewer (attn_plan)
 constexpr int ATT_BS = 16;             // tokens per page
 
-template <typename T> struct AttnT;
-template <> struct AttnT<bf16_t> {
-  static constexpr int KPL = 8;        // elements per lane per MFMA slot
+// Arithmetic of the register-staged kernel. QKPL / PKPL: elements a lane supplies per MFMA slot for the
+// scores and for the weighted V sum.
+// fp32 inputs: fp32 MFMA for both products.
+struct AttnF32 {
+  typedef float T;
+  static constexpr int QKPL = 1, PKPL = 1;
+  typedef float qfrag;
+  typedef float vt;                    // V^T element in LDS
+  typedef float pfrag;
+  static __device__ __forceinline__ f32x16 mma_qk(qfrag a, qfrag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ f32x16 mma_pv(pfrag a, pfrag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+// bf16 inputs for any V: bf16 MFMA for the scores (as the DMA kernel), V widened exactly to fp32 and the
+// weighted sum on fp32 MFMA with P in fp32.
+struct AttnBf16Wide {
+  typedef bf16_t T;
+  static constexpr int QKPL = 8, PKPL = 1;
   typedef u32x4 qfrag;                 // 8 x bf16
-  typedef _Float16 vt;                 // V^T element in LDS
-  typedef f16x8 pfrag;
-  static constexpr int PADK = 8, PADV = 4;
+  typedef float vt;
+  typedef float pfrag;
   static __device__ __forceinline__ f32x16 mma_qk(qfrag a, qfrag b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                    0, 0, 0);
-  }
-  static __device__ __forceinline__ f32x16 mma_pv(pfrag a, pfrag b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
-  }
-};
-template <> struct AttnT<float> {
-  static constexpr int KPL = 1;
-  typedef float qfrag;
-  typedef float vt;
-  typedef float pfrag;
-  static constexpr int PADK = 4, PADV = 4;
-  static __device__ __forceinline__ f32x16 mma_qk(qfrag a, qfrag b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ f32x16 mma_pv(pfrag a, pfrag b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
@@ -70,13 +84,13 @@ __device__ __forceinline__ int tile_row(int i, int h) { return 8 * (i >> 2) + 4 
 // conflicts.
 __device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 2)) & 15; }
 
-template <typename T, int D>
+template <class AT, int D>
 struct AttnGeom {
-  static constexpr int E = sizeof(T);                    // element bytes in the cache
+  static constexpr int E = sizeof(typename AT::T);       // element bytes in the cache
   static constexpr int ROWB = D * E;                     // bytes of one K row
   static constexpr int NCH = ROWB / 16;                  // 16-byte chunks per K row
   static constexpr int KTILE = ATT_KT * ROWB;            // bytes of a K tile
-  static constexpr int VE = sizeof(typename AttnT<T>::vt);
+  static constexpr int VE = sizeof(typename AT::vt);
   static constexpr int VROWB = ATT_KT * VE;              // bytes of one V^T row (64 keys)
   static constexpr int VTILE = D * VROWB;
   static constexpr int NT = ATT_NW * 64;
@@ -88,12 +102,14 @@ struct AttnGeom {
 };
 
 // Per-block metadata of one work item: the byte offset of every prefix page of the chunk (this KV
-// head), the tree's parents and ancestor masks (last chunk only) and an input-error flag.
+// head), the tree's parents and ancestor masks (last chunk only), an input-error flag and (DMA kernel)
+// the flag of a V value outside fp16's exact range.
 struct AttnMeta {
   long long pgoff[ATT_CHUNK_PAGES];
   uint32_t anc[SR_MAX_TREE][SR_MAX_TREE / 32];
   int parent[SR_MAX_TREE];
   int bad;
+  int vwide;
 };
 
 // Fills AttnMeta for pages [page0, page1) of trajectory b and, for the last chunk, its tree; validates
@@ -102,7 +118,7 @@ template <int D, int E>
 __device__ bool attn_meta(AttnMeta& m, bool ctx_ok, bool last, int page0, int page1, const int32_t* bt_b,
                           const int32_t* par_b, int T_, int Hkv, int g, int num_blocks) {
   const int tid = threadIdx.x, nt = blockDim.x;
-  if (tid == 0) m.bad = ctx_ok ? 0 : 1;
+  if (tid == 0) { m.bad = ctx_ok ? 0 : 1; m.vwide = 0; }
   __syncthreads();
   for (int p = page0 + tid; p < page1; p += nt) {
     int blk = bt_b[p];
@@ -128,42 +144,42 @@ __device__ bool attn_meta(AttnMeta& m, bool ctx_ok, bool last, int page0, int pa
   return m.bad != 0;
 }
 
-template <typename T, int D>
+template <class AT, int D>
 struct AttnSmem {
-  using G = AttnGeom<T, D>;
+  using G = AttnGeom<AT, D>;
   __attribute__((aligned(16))) unsigned char k[2][G::KTILE];
   __attribute__((aligned(16))) unsigned char v[2][G::VTILE];
   AttnMeta meta;
 };
 
 // registers holding one tile's K and V while the previous tile is being computed
-template <typename T, int D>
+template <class AT, int D>
 struct TileRegs {
-  using G = AttnGeom<T, D>;
+  using G = AttnGeom<AT, D>;
   u32x4 k[G::KVPT];
   uint32_t v[G::VIPT][4][G::E];  // per item: 4 keys x (4 dims x E bytes)
 };
 
-template <typename T, int D>
-__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
-    const T* __restrict__ q, const T* __restrict__ k_cache, const T* __restrict__ v_cache,
-    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const T* __restrict__ k_tree,
-    const T* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
-    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
-    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int n_chunks_max,
-    int cp) {
-  using AT = AttnT<T>;
-  using G = AttnGeom<T, D>;
-  constexpr int KPL = AT::KPL, KSTEP = 2 * KPL;
+// Work item (trajectory b, KV head g, chunk c, row group rg) of the register-staged path, rows
+// [rg group_rows, min(R, (rg + 1) group_rows)) with group_rows <= ATT_ROWS. Whole block.
+template <class AT, int D>
+__device__ __forceinline__ void attn_item_regs(
+    AttnSmem<AT, D>& sm, int b, int g, int c, int rg, const typename AT::T* __restrict__ q,
+    const typename AT::T* __restrict__ k_cache, const typename AT::T* __restrict__ v_cache,
+    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len,
+    const typename AT::T* __restrict__ k_tree, const typename AT::T* __restrict__ v_tree,
+    const int32_t* __restrict__ parents, float* __restrict__ out, float* __restrict__ lse,
+    float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv, int max_blocks,
+    int num_blocks, float scale_log2, int R, int Rpad, int group_rows, int n_chunks_max, int cp) {
+  using T = typename AT::T;
+  using G = AttnGeom<AT, D>;
+  constexpr int QKPL = AT::QKPL, KSTEP = 2 * QKPL, PKPL = AT::PKPL;
   constexpr int NQF = D / KSTEP;      // Q fragments per lane and row block
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
   constexpr int NT = G::NT;
   constexpr int RB = ATT_RB;
-  __shared__ AttnSmem<T, D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-  const int rg = blockIdx.x % row_groups, bg = blockIdx.x / row_groups;
-  const int g = bg % Hkv, b = bg / Hkv, c = blockIdx.y;
   const int G_ = Hq / Hkv;
   const int Lraw = ctx_len[b];
   const bool ctx_ok = Lraw >= 0 && Lraw <= max_blocks * ATT_BS;
@@ -180,7 +196,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
                                            parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
 
   // ---- this wave's query rows: row r <-> (node t = r / G, head g*G + r % G); RB blocks of 32
-  const int wrow0 = rg * ATT_ROWS + wave * RB * 32;
+  const int rend = min(R, (rg + 1) * group_rows);
+  const int wrow0 = rg * group_rows + wave * RB * 32;
   int my_r[RB], my_t[RB];
   bool row_ok[RB];
   typename AT::qfrag qf[RB][NQF];
@@ -188,13 +205,13 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     my_r[rb] = wrow0 + rb * 32 + (lane & 31);
-    row_ok[rb] = my_r[rb] < R;
+    row_ok[rb] = my_r[rb] < rend;
     my_t[rb] = row_ok[rb] ? my_r[rb] / G_ : 0;
     const T* qp = q + (((size_t)b * T_ + my_t[rb]) * Hq + g * G_ + (row_ok[rb] ? my_r[rb] % G_ : 0)) * D;
 #pragma unroll
     for (int kq = 0; kq < NQF; ++kq) {
-      const int dd = kq * KSTEP + half * KPL;
-      if constexpr (KPL == 8) {
+      const int dd = kq * KSTEP + half * QKPL;
+      if constexpr (QKPL == 8) {
         u32x4 z = {0, 0, 0, 0};
         if (row_ok[rb]) z = *(const u32x4*)(qp + dd);
         qf[rb][kq] = z;
@@ -215,7 +232,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
     m_run[rb] = -INFINITY;
     l_run[rb] = 0.f;
   }
-  const bool wave_active = wrow0 < R && !bad;
+  const bool wave_active = wrow0 < rend && !bad;
 
   // ---- tile schedule: prefix tiles of this chunk, then (last chunk) the tree tiles
   const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
@@ -230,7 +247,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   const unsigned char* vt_b = (const unsigned char*)(v_tree + ((size_t)b * T_ * Hkv + g) * D);
   const int tree_rowb = Hkv * G::ROWB;                                  // bytes between tree nodes
   auto load_tile = [&](const unsigned char* kb, const unsigned char* vb, int t0, int lim, auto off_of,
-                       TileRegs<T, D>& r) {
+                       TileRegs<AT, D>& r) {
 #pragma unroll
     for (int j = 0; j < G::KVPT; ++j) {
       const int vi = tid + j * NT;
@@ -257,7 +274,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
       }
     }
   };
-  auto fetch = [&](int i, TileRegs<T, D>& r) {
+  auto fetch = [&](int i, TileRegs<AT, D>& r) {
     if (i < n_pre) {
       load_tile(kc_b, vc_b, key0 + i * ATT_KT, key1,
                 [&](int kidx) -> long long { return sm.meta.pgoff[(kidx >> 4) - page0] + (kidx & 15) * G::ROWB; }, r);
@@ -266,8 +283,9 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
                 r);
     }
   };
-  // registers -> LDS stage (K row-major with chunk swizzle, V transposed with group swizzle)
-  auto stash = [&](int st, const TileRegs<T, D>& r) {
+  // registers -> LDS stage (K row-major with chunk swizzle, V transposed with group swizzle; bf16 V is
+  // widened to the fp32 V^T element exactly)
+  auto stash = [&](int st, const TileRegs<AT, D>& r) {
 #pragma unroll
     for (int j = 0; j < G::KVPT; ++j) {
       const int vi = tid + j * NT;
@@ -283,59 +301,48 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
       for (int i = 0; i < 4; ++i) {
         const int d = dg * 4 + i;
         unsigned char* dst = sm.v[st] + d * G::VROWB + ((kg ^ vswz(d)) * 4 * G::VE);
-        if constexpr (G::E == 2) {
-          f16x4 h;
+        f32x4 h;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < 4; ++j) {
+          if constexpr (G::E == 2) {
             const uint32_t w = r.v[it][j][i >> 1];
-            h[j] = (_Float16)bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+            h[j] = bf2f((i & 1) ? (w >> 16) : (w & 0xffffu));
+          } else {
+            h[j] = __uint_as_float(r.v[it][j][i]);
           }
-          *(f16x4*)dst = h;
-        } else {
-          f32x4 h;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) h[j] = __uint_as_float(r.v[it][j][i]);
-          *(f32x4*)dst = h;
         }
+        *(f32x4*)dst = h;
       }
     }
   };
+  static_assert(G::VE == 4, "V^T is staged as fp32");
 
   auto compute = [&](int i, int st) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
     const unsigned char* ks_ = sm.k[st];
     const unsigned char* vs_ = sm.v[st];
-    // scores S^T: each K fragment feeds both row blocks
+    // scores S^T: each K fragment feeds every row block
     f32x16 s[RB][2];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = (f32x16){};
 #pragma unroll
     for (int kq = 0; kq < NQF; ++kq) {
-      const int e = kq * KSTEP + half * KPL;            // first element this lane supplies
+      const int e = kq * KSTEP + half * QKPL;           // first element this lane supplies
       const int ch = (e * G::E) / 16;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const int key = kt * 32 + (lane & 31);
         const unsigned char* p = ks_ + key * G::ROWB + ((ch ^ (key & (G::NCH - 1))) * 16) + (e * G::E) % 16;
         typename AT::qfrag kf;
-        if constexpr (KPL == 8) kf = *(const u32x4*)p; else kf = *(const float*)p;
+        if constexpr (QKPL == 8) kf = *(const u32x4*)p; else kf = *(const float*)p;
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) s[rb][kt] = AT::mma_qk(kf, qf[rb][kq], s[rb][kt]);
       }
     }
-    // interleave the K fragment reads with the score MFMAs (4 reads ahead, then 2 reads per 2 MFMAs)
-    if constexpr (KPL == 8) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-      for (int q = 0; q < 6; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    }
     // online softmax per row block; vis holds one bit per key of each 32-key subtile, pre-shifted by
     // this lane half's row offset
-    typename AT::pfrag pf[RB][2][16 / KPL];
+    typename AT::pfrag pf[RB][2][16 / PKPL];
     const bool full = !tree && t0 + ATT_KT <= key1;      // every key of the tile is visible to every row
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -368,8 +375,8 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[rb][kt][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // the reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
-      // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled
+      // the reference max moves only when the tile max exceeds it by more than 2^8 (P in [0, 256]), so
+      // the accumulator is rarely rescaled
       const float tmax = mx * scale_log2;
       const float m_new = (tmax > m_run[rb] + 8.f) ? tmax : m_run[rb];
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
@@ -381,8 +388,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
         for (int r = 0; r < 16; ++r) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][kt][r], scale_log2, -m_use));
           psum += p;
-          if constexpr (KPL == 8) pf[rb][kt][r >> 3][r & 7] = (_Float16)p;
-          else pf[rb][kt][r] = p;
+          pf[rb][kt][r] = p;
         }
       l_run[rb] = l_run[rb] * alpha + psum;
       m_run[rb] = m_new;
@@ -391,44 +397,27 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
         for (int dt = 0; dt < NDT; ++dt) o[rb][dt] *= alpha;
       }
     }
-    // O^T += V^T P^T; each V fragment feeds both row blocks
+    // O^T += V^T P^T; each V fragment feeds every row block
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int kq = 0; kq < 16 / KPL; ++kq) {
+      for (int kq = 0; kq < 16 / PKPL; ++kq) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
           const int d = dt * 32 + (lane & 31);
           const unsigned char* vrow = vs_ + d * G::VROWB;
           const int sw = vswz(d);
-          typename AT::pfrag vf;
-          if constexpr (KPL == 8) {
-            const int g0 = (kt * 32 + tile_row(kq * 8, half)) >> 2;      // 4 consecutive keys
-            const f16x4 lo = *(const f16x4*)(vrow + ((g0 ^ sw) * 8));
-            const f16x4 hi = *(const f16x4*)(vrow + (((g0 + 2) ^ sw) * 8));
-            vf = (f16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          } else {
-            const int key = kt * 32 + tile_row(kq, half);
-            vf = *(const float*)(vrow + (((key >> 2) ^ sw) * 16) + (key & 3) * 4);
-          }
+          const int key = kt * 32 + tile_row(kq, half);
+          const float vf = *(const float*)(vrow + (((key >> 2) ^ sw) * 16) + (key & 3) * 4);
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) o[rb][dt] = AT::mma_pv(vf, pf[rb][kt][kq], o[rb][dt]);
         }
       }
-    // interleave the V fragment reads with the PV MFMAs (8 reads ahead, then 2 reads per MFMA)
-    if constexpr (KPL == 8) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-      for (int q = 0; q < 12; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    }
   };
 
   // ---- software pipeline: tile i+1 is in flight (registers) while tile i is computed from LDS
   if (n_tiles > 0) {
-    TileRegs<T, D> regs;
+    TileRegs<AT, D> regs;
     fetch(0, regs);
     stash(0, regs);
     __syncthreads();
@@ -483,6 +472,47 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
   }
 }
 
+// fp32 inputs: one block per item, grid (B Hkv row_groups, chunks).
+template <int D>
+__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn(
+    const float* __restrict__ q, const float* __restrict__ k_cache, const float* __restrict__ v_cache,
+    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const float* __restrict__ k_tree,
+    const float* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int T_, int Hq, int Hkv,
+    int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
+    int n_chunks_max, int cp) {
+  __shared__ AttnSmem<AttnF32, D> sm;
+  const int rg = blockIdx.x % row_groups, bg = blockIdx.x / row_groups;
+  attn_item_regs<AttnF32, D>(sm, bg / Hkv, bg % Hkv, blockIdx.y, rg, q, k_cache, v_cache, block_table, ctx_len,
+                             k_tree, v_tree, parents, out, lse, part_o, part_ml, T_, Hq, Hkv, max_blocks, num_blocks,
+                             scale_log2, R, Rpad, group_rows, n_chunks_max, cp);
+}
+
+// bf16 items that k_tree_attn_dma listed (a V value outside fp16's exact range), recomputed with V in
+// fp32. redo[0] = count, redo[1..] = item indices ((c B + b) Hkv + g) row_groups + rg. The loop bound
+// is read once per block and is uniform, so every wave runs the same iterations.
+template <int D>
+__global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_redo(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache, const bf16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ block_table, const int32_t* __restrict__ ctx_len, const bf16_t* __restrict__ k_tree,
+    const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
+    int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
+    int n_chunks_max, int cp, int n_items, const unsigned* __restrict__ redo) {
+  __shared__ AttnSmem<AttnBf16Wide, D> sm;
+  const int n = min((int)__builtin_amdgcn_readfirstlane(redo[0]), n_items);
+  for (int k = blockIdx.x; k < n; k += gridDim.x) {
+    const int item = (int)__builtin_amdgcn_readfirstlane(redo[1 + k]);
+    if (item < 0 || item >= n_items) continue;   // uniform
+    const int rg = item % row_groups, bg = item / row_groups;
+    const int g = bg % Hkv, b = (bg / Hkv) % B_, c = bg / (Hkv * B_);
+    __syncthreads();                              // the previous item's LDS reads are done
+    attn_item_regs<AttnBf16Wide, D>(sm, b, g, c, rg, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree,
+                                    parents, out, lse, part_o, part_ml, T_, Hq, Hkv, max_blocks, num_blocks,
+                                    scale_log2, R, Rpad, group_rows, n_chunks_max, cp);
+  }
+}
+
 // ============================================================================ bf16, direct-to-LDS
 // The bf16 path streams K and V tiles from HBM straight into LDS (global_load_lds_dwordx4) through a
 // four-slot ring: while tile i is finished and tile i+1 prepared, tiles i+2 and i+3 are in flight. In LDS,
@@ -503,7 +533,7 @@ struct DmaGeom {
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
   static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
   static constexpr int CPL = (CITEMS + 7 * 64 - 1) / (7 * 64);   // chunks per lane with >= 7 converting waves
-  static_assert(BLK % ATT_NW == 0 && CITEMS % 64 == 0, "tile split");
+  static_assert(CITEMS % 64 == 0, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
 };
@@ -518,22 +548,15 @@ __device__ __forceinline__ float max_halves(float x) {
 // take four different 64-byte column groups
 template <int NCH> __device__ __forceinline__ int vswz(int k) { return (4 * (k & 3)) & (NCH - 1); }
 
-// Complete this wave's LDS writes and its DMA for the next tile, then meet the block. A wave that
-// issues DMA (one of npd such waves, each with 2*BLK/npd transfers per tile) may leave the transfers
-// of the tile after that in flight when `ahead`.
+// Complete this wave's LDS writes and its DMA for the next tile, then meet the block. The DMA wave (2 BLK
+// transfers per tile) may leave the transfers of the tile after that in flight when `ahead`.
 template <int D>
-__device__ __forceinline__ void attn_sync(int npd, bool dma_wave, bool ahead) {
+__device__ __forceinline__ void attn_sync(bool dma_wave, bool ahead) {
   constexpr int BLK = DmaGeom<D>::BLK;
   if (!dma_wave || !ahead) {
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  } else if (npd == 1) {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * BLK) : "memory");
-  } else if (npd == 2) {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK) : "memory");
-  } else if (npd == 4) {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK / 2) : "memory");
   } else {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(BLK / 4) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * BLK) : "memory");
   }
 }
 
@@ -548,7 +571,7 @@ __device__ __forceinline__ void attn_item_dma(
     const bf16_t* __restrict__ v_tree, const int32_t* __restrict__ parents, float* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
     int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
-    int n_chunks_max, int cp) {
+    int n_chunks_max, int cp, unsigned* __restrict__ redo) {
   using G = DmaGeom<D>;
   constexpr int NQF = D / 16;         // Q fragments per lane
   constexpr int NDT = D / 32;         // 32-wide output tiles along D
@@ -594,16 +617,14 @@ __device__ __forceinline__ void attn_item_dma(
 #pragma unroll
   for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
   float m_run = -INFINITY, l_run = 0.f;
-  // Roles. Without any wave free of query rows, all waves share the DMA and the V conversion. Else
-  // the first row-free wave issues all of the DMA (npd = 1), pacing itself on the memory system, and
-  // the other waves convert V (a single converting wave would hold the block at the barrier).
-  const int n_act = min(ATT_NW, (rend - rg * group_rows + 31) / 32);
-  const int n_prod = ATT_NW - n_act;
+  // Roles. A row group holds at most ATT_ROWS - 32 rows (attn_plan), so wave n_act has no query rows: it
+  // issues all of the DMA, pacing itself on the memory system, and the other seven waves convert V (a
+  // single converting wave would hold the block at the barrier).
+  const int n_act = min(ATT_NW - 1, (rend - rg * group_rows + 31) / 32);
   const bool wave_active = wave < n_act && !bad;
-  const int npd = n_prod == 0 ? ATT_NW : 1;
-  const bool dma_wave = n_prod == 0 || wave == n_act;
-  const int n_tr = n_prod == 0 ? ATT_NW : ATT_NW - 1;
-  const int tr_rank = (n_prod == 0 || wave < n_act) ? wave : (wave == n_act ? -1 : wave - 1);
+  const bool dma_wave = wave == n_act;
+  constexpr int n_tr = ATT_NW - 1;
+  const int tr_rank = wave < n_act ? wave : (wave == n_act ? -1 : wave - 1);
 
   const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
   const int n_tiles = bad ? 0 : n_pre + (last ? (T_ + ATT_KT - 1) / ATT_KT : 0);
@@ -634,17 +655,6 @@ __device__ __forceinline__ void attn_item_dma(
     const long long base = tree ? (long long)(kt_b - kc_b) : 0;   // tree rows are addressed from kc_b
     ko = base + off + ((pos ^ (kk & (G::NCH - 1))) * 16);
     vo = (tree ? (long long)(vt_b - vc_b) : 0) + off + ((pos ^ vswz<G::NCH>(kk)) * 16);
-  };
-  // every wave issues its BLK/8 blocks of K and of V (all waves have query rows)
-  auto issue_dist = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < G::BLK / ATT_NW; ++j) {
-      const int blk = wave + j * ATT_NW;
-      long long ko, vo;
-      block_src(i, blk, ko, vo);
-      lds_dma16_manual(kc_b + ko, slot + blk * 1024);
-      lds_dma16_manual(vc_b + vo, slot + G::TILE + blk * 1024);
-    }
   };
   // one producer wave issues the whole tile. A full prefix tile is four whole pages: each page's K and V
   // bases are uniform (scalar registers) and a block's per-lane offset inside its page depends only on
@@ -690,14 +700,15 @@ __device__ __forceinline__ void attn_item_dma(
       }
     }
   };
-  auto issue = [&](int i, unsigned char* slot) __attribute__((always_inline)) {
-    if (n_prod == 0) issue_dist(i, slot);
-    else issue_prod(i, slot);
-  };
+  auto issue = [&](int i, unsigned char* slot) __attribute__((always_inline)) { issue_prod(i, slot); };
   // V of a tile, bf16 -> fp16 in place: every converting lane takes whole 16-byte chunks (their positions
   // do not matter). The reads (conv_load) are issued early and the converted chunks written later
-  // (conv_store), so the LDS latency overlaps other work.
+  // (conv_store), so the LDS latency overlaps other work. The conversion is exact for a zero and for
+  // magnitudes in [2^-14, 65280] (bf16 patterns 0x3880..0x477f without the sign); each converting lane
+  // keeps the largest magnitude pattern and the smallest nonzero one (minus one, so zero wraps to 0xffff)
+  // of everything it converts, two 16-bit lanes per register.
   u32x4 cw[G::CPL];
+  u16x2 vmag_hi = {0, 0}, vmag_lo = {0xffff, 0xffff};
   auto conv_load = [&](const unsigned char* v) __attribute__((always_inline)) {
     if (tr_rank < 0) return;                    // the DMA wave
     int ln = lane;
@@ -721,6 +732,12 @@ __device__ __forceinline__ void attn_item_dma(
         for (int e = 0; e < 8; ++e)
           h[e] = (_Float16)bf2f((e & 1) ? (cw[k][e >> 1] >> 16) : (cw[k][e >> 1] & 0xffffu));
         *(f16x8*)(v + it * 16) = h;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const u16x2 mag = __builtin_bit_cast(u16x2, cw[k][w] & 0x7fff7fffu);
+          vmag_hi = __builtin_elementwise_max(vmag_hi, mag);
+          vmag_lo = __builtin_elementwise_min(vmag_lo, mag - (u16x2){1, 1});
+        }
       }
     }
   };
@@ -862,7 +879,7 @@ __device__ __forceinline__ void attn_item_dma(
   f32x16 sa[2], sb[2];
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
     const int sn_ = (si + 1) & 3, sf = (si + 3) & 3;
-    attn_sync<D>(npd, dma_wave, i + 2 < n_tiles);
+    attn_sync<D>(dma_wave, i + 2 < n_tiles);
     if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[sf]);
     const bool cv = i + 1 < n_tiles;
     if (cv) conv_load(ring[sn_] + G::TILE);
@@ -876,7 +893,7 @@ __device__ __forceinline__ void attn_item_dma(
       issue(0, ring[0]);
       if (n_tiles > 1) issue(1, ring[1]);
     }
-    attn_sync<D>(npd, dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
+    attn_sync<D>(dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
     if (dma_wave && n_tiles > 2) issue(2, ring[2]);
     conv_load(ring[0] + G::TILE);
     conv_store(ring[0] + G::TILE);
@@ -889,6 +906,19 @@ __device__ __forceinline__ void attn_item_dma(
         step(i + 1, si, sb, sa);
         si = (si + 1) & 3;
       }
+    }
+  }
+
+  // ---- a V value outside fp16's exact range: list the item for the fp32-V recomputation (its outputs
+  // written below are then overwritten before anything reads them)
+  {
+    const uint32_t hi = max((uint32_t)vmag_hi[0], (uint32_t)vmag_hi[1]);
+    const uint32_t lo = min((uint32_t)vmag_lo[0], (uint32_t)vmag_lo[1]);
+    if (__ballot(hi > 0x477fu || lo < 0x387fu) != 0 && lane == 0) atomicOr(&meta.vwide, 1);
+    __syncthreads();
+    if (threadIdx.x == 0 && meta.vwide != 0) {
+      const unsigned k = atomicAdd(redo, 1u);
+      redo[1 + k] = (unsigned)item;
     }
   }
 
@@ -942,6 +972,7 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
     int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
     int n_chunks_max, int cp, int n_items, unsigned* __restrict__ work) {
+  // work[0]: item counter; work[1], work[2..]: count and items of the fp32-V redo list
   __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * DmaGeom<D>::TILE];
   __shared__ AttnMeta meta;
   __shared__ int s_item;
@@ -953,12 +984,12 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     if (item >= n_items) break;
     attn_item_dma<D>(item, ring, meta, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out,
                      lse, part_o, part_ml, B_, T_, Hq, Hkv, max_blocks, num_blocks, scale_log2, R, Rpad,
-                     row_groups, group_rows, n_chunks_max, cp);
+                     row_groups, group_rows, n_chunks_max, cp, work + 1);
   }
 }
 
 __global__ void k_attn_work_reset(unsigned* __restrict__ work) {
-  if (threadIdx.x == 0) *work = 0u;
+  if (threadIdx.x < 2) work[threadIdx.x] = 0u;   // item counter, redo count
 }
 
 // Merge the chunk partials of every (trajectory, KV head) that was split.
@@ -1032,10 +1063,10 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   AttnPlan p;
   p.R = d.T * (d.Hq / d.Hkv);
   p.Rpad = (p.R + 31) / 32 * 32;
-  // bf16: more than one block's rows split evenly into groups of at most 224 rows, so every work item
-  // keeps a wave free of query rows to issue its DMA (fp32: groups of 256)
+  // bf16: more than 224 rows split evenly into groups of at most 224, so every work item keeps a wave
+  // free of query rows to issue its DMA (fp32: groups of 256)
   p.group_rows = ATT_ROWS;
-  if (d.dtype == SR_BF16 && p.R > ATT_ROWS) {
+  if (d.dtype == SR_BF16 && p.R > ATT_ROWS - 32) {
     const int ng = (p.R + (ATT_ROWS - 32) - 1) / (ATT_ROWS - 32);
     p.group_rows = ((p.R + ng - 1) / ng + 31) / 32 * 32;
   }
@@ -1049,7 +1080,9 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   const size_t rows = (size_t)d.B * d.Hkv * p.n_chunks * p.Rpad;
   p.part_o_bytes = p.n_chunks > 1 ? rows * d.D * sizeof(float) : 0;
   p.part_ml_bytes = p.n_chunks > 1 ? rows * 2 * sizeof(float) : 0;
-  p.work_bytes = d.dtype == SR_BF16 ? sizeof(unsigned) : 0;   // work-item counter of the persistent kernel
+  // bf16: the persistent kernel's item counter, then the count and items of the fp32-V redo list
+  p.n_items = (long long)d.B * d.Hkv * p.row_groups * p.n_chunks;
+  p.work_bytes = d.dtype == SR_BF16 ? (size_t)(2 + p.n_items) * sizeof(unsigned) : 0;
   return p;
 }
 
@@ -1086,10 +1119,17 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.B, d.T, d.Hq, d.Hkv,
               d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.group_rows, p.n_chunks,
               p.chunk_pages, (int)n_items, work);
+    // items holding a V value outside fp16's exact range, recomputed with fp32 V (blocks exit at once when
+    // the list is empty)
+    SR_LAUNCH("sr_attn_redo", (k_tree_attn_redo<D>), dim3(nb), dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
+              (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.B, d.T, d.Hq, d.Hkv,
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.group_rows, p.n_chunks,
+              p.chunk_pages, (int)n_items, (const unsigned*)(work + 1));
   } else {
-    SR_LAUNCH("sr_tree_attn", (k_tree_attn<T, D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
+    SR_LAUNCH("sr_tree_attn", (k_tree_attn<D>), grid, dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.T, d.Hq, d.Hkv,
-              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.n_chunks, p.chunk_pages);
+              d.max_blocks, d.num_blocks, scale_log2, p.R, p.Rpad, p.row_groups, p.group_rows, p.n_chunks,
+              p.chunk_pages);
   }
   if (p.n_chunks > 1) {
     constexpr int RPB = 256 / (D / 4);

@@ -31,7 +31,8 @@ struct AttnPlan {
   int chunk_pages;  // prefix pages per work item
   int n_chunks;     // work items per (trajectory, KV head), worst case
   size_t part_o_bytes, part_ml_bytes;
-  size_t work_bytes;  // work-item counter (bf16 path)
+  long long n_items;  // work items (trajectory, KV head, row group, chunk)
+  size_t work_bytes;  // bf16: item counter, then the redo count and list (2 + n_items words)
 };
 AttnPlan attn_plan(const sr_attn_desc& d);
 sr_status launch_tree_attn(const sr_attn_desc& d, const AttnPlan& p, const void* q, const void* k_cache,
