@@ -80,7 +80,10 @@ struct AccSmem {
   double cscale[ACC_MAX_CHUNKS];
   int kids[SR_MAX_TREE];
   double kpt[SR_MAX_TREE];   // unnormalised target weight of each child's token at the current node
+  double xsum[ACC_MAX_CHUNKS];         // chunks holding a child: the weight of their other tokens
+  unsigned char xflag[ACC_MAX_CHUNKS]; // the chunk holds a child of the current node
   double S;
+  double S_out;      // weight of the row outside the current node's children
   int bad;
   int nkid;
   int accepted;      // slot index (0-based) accepted at the current node, -1 = all rejected
@@ -503,8 +506,65 @@ __device__ void nuc_masked_sums(AccSmem& sm, const T* __restrict__ row, int V, f
   __syncthreads();
 }
 
+// Weight of the current row outside the node's m children (sm.kids), chunk by chunk. A chunk that holds a
+// child is summed again over its other tokens: its chunk sum minus the children's weights would keep only
+// fp32 rounding of the remainder when the children hold most of the chunk (peaked rows). Sets xflag and
+// xsum of those chunks and sm.S_out; with the nucleus cut also sm.S, the sum of the (nucleus-masked) chunk
+// sums. Whole block.
+template <typename T, bool NUC>
+__device__ void outside_mass(AccSmem& sm, const T* __restrict__ row, int V, float invtau, int m) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  for (int c = tid; c < nch; c += ACC_NT) sm.xflag[c] = 0;
+  __syncthreads();
+  for (int k = tid; k < m; k += ACC_NT) sm.xflag[sm.tok[sm.kids[k]] / ACC_CH] = 1;
+  __syncthreads();
+  for (int k = wave; k < m; k += ACC_NW) {
+    const int c = sm.tok[sm.kids[k]] / ACC_CH;
+    bool first = true;                           // the first child of its chunk sums it
+    for (int k2 = 0; k2 < k; ++k2)
+      if (sm.tok[sm.kids[k2]] / ACC_CH == c) { first = false; break; }
+    if (!first) continue;                        // uniform per wave
+    const int base = c * ACC_CH + lane * 8;
+    unsigned excl = 0;                           // this lane's tokens that are children
+    for (int k2 = 0; k2 < m; ++k2) {
+      const int v = sm.tok[sm.kids[k2]];
+      if (v >= base && v < base + 8) excl |= 1u << (v - base);
+    }
+    double s = 0.0;
+    if (base < V) {                              // V is a multiple of 8: all 8 tokens are in the row
+      float x[8];
+      RowLoad<T>::load8(row + base, x);
+      const float cm = sm.cmax[c];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (!((excl >> e) & 1u) && x[e] != -INFINITY && nuc_member(sm, x[e], base + e))
+          s += (double)tilt(x[e], invtau, cm);
+    }
+    s = wave_sum_f64(s);
+    if (lane == 0) sm.xsum[c] = s * sm.cscale[c];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    double so = 0.0, st = 0.0;
+    for (int c = lane; c < nch; c += 64) {
+      const double a = sm.csum[c] * sm.cscale[c];
+      st += a;
+      so += sm.xflag[c] ? sm.xsum[c] : a;
+    }
+    so = wave_sum_f64(so);
+    st = wave_sum_f64(st);
+    if (lane == 0) {
+      sm.S_out = so;
+      if (NUC) sm.S = st;
+    }
+  }
+  __syncthreads();
+}
+
 // Inverse-CDF draw over the current row, token-id order, excluding the tokens of
-// sm.kids[0..n_excl). Run by wave 0; result in sm.draw_tok / sm.draw_margin.
+// sm.kids[0..n_excl) (whose chunks' remaining weights outside_mass left in xsum). Run by wave 0; result in
+// sm.draw_tok / sm.draw_margin.
 template <typename T>
 __device__ void draw(AccSmem& sm, const T* __restrict__ row, int V, float invtau, int n_excl, float U) {
   const int lane = threadIdx.x & 63;
@@ -517,12 +577,7 @@ __device__ void draw(AccSmem& sm, const T* __restrict__ row, int V, float invtau
   for (int i = 0; i < CPL; ++i) {
     const int c = lane * CPL + i;
     double a = 0.0;
-    if (c < nch) {
-      a = sm.csum[c] * sm.cscale[c];
-      for (int k = 0; k < n_excl; ++k)          // the children's weights, kept by the node's slot tests
-        if (sm.tok[sm.kids[k]] / ACC_CH == c) a -= sm.kpt[k];
-      a = fmax(a, 0.0);
-    }
+    if (c < nch) a = (n_excl > 0 && sm.xflag[c]) ? sm.xsum[c] : sm.csum[c] * sm.cscale[c];
     adj[i] = a;
     lsum += a;
   }
@@ -697,6 +752,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
       row_stats_nuc<T>(sm, row, V, invtau);
       nucleus<T>(sm, row, V, invtau, top_p);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
+      nuc_masked_sums<T>(sm, row, V, invtau);   // chunk sums over the nucleus; outside_mass sums them to S
     } else {
       row_stats<T>(sm, row, V, invtau);
     }
@@ -708,10 +764,10 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     }
     __syncthreads();
     const int m = sm.nkid;
+    outside_mass<T, NUC>(sm, row, V, invtau, m);
     if (wave == 0) {
       // residual on the children (2 per lane) and the mass outside them, float64
       double r[2], lg[2];
-      double out_mass_part = 0.0;
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         const int k = lane + 64 * s;
@@ -722,10 +778,9 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
           sm.kpt[k] = pt;
           r[s] = pt / sm.S;
           lg[s] = (double)sm.cl[sm.kids[k]];
-          out_mass_part += pt;
         }
       }
-      double rest = (sm.S - wave_sum_f64(out_mass_part)) / sm.S;
+      double rest = sm.S_out / sm.S;
       int acc = -1;
       for (int j = 0; j < m; ++j) {
         // q_{u,j}: softmax of the draft logits over children j..m-1
@@ -768,7 +823,6 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     const int acc = sm.accepted;
     if (acc < 0) {
       // every child rejected: fallback from the final residual = p outside the children
-      if constexpr (NUC) nuc_masked_sums<T>(sm, row, V, invtau);
       if (wave == 0) draw<T>(sm, row, V, invtau, m, Ufin);
       __syncthreads();
       if (tid == 0) {

@@ -108,6 +108,81 @@ def test_full_size_sampled(name, rseed):
     _compare(inp, rows=rows)
 
 
+@pytest.mark.parametrize("point", synth.SWEEP_POINTS, ids=lambda p: f"B{p[0]}-T{p[1]}")
+def test_sweep_points_sampled(point):
+    # the concurrency sweep at full vocabulary: trees of 8 to 96 nodes (the 96-node root has 32 children)
+    cfg = synth.sweep_config(*point)
+    inp = synth.accept_inputs(cfg, seed=0)
+    rows = np.random.default_rng(point[1]).choice(cfg.B, size=min(8, cfg.B), replace=False)
+    _compare(inp, rows=rows)
+
+
+def test_largest_tree():
+    # SR_MAX_TREE = 128 nodes at depth 6 (the root has 43 children), every trajectory compared
+    cfg = synth.scaled(synth.SHAPE_7B, B=24, T=128, depth=6, V=4096)
+    _compare(synth.accept_inputs(cfg, seed=15))
+    g, _ = _compare(synth.accept_inputs(cfg, seed=16, target_std=8.0, noise_std=0.05))
+    assert g["out_len"].max() >= 3
+
+
+def _peaked_inputs(B, V, seed, p_child=0.999, secondary=0):
+    """Trajectories whose root target row puts mass ~p_child on the two drafted children, with slot uniforms above
+    the acceptance ratios so both children are rejected: the fallback draws from the ~1 - p_child of mass outside
+    the children, whose chunk sums must not be taken as differences of the large chunk sums holding the
+    children. With ``secondary`` > 0 that many other tokens hold 90 % of the outside mass (so a nucleus cut can
+    fall among them instead of among tail tokens of ~1e-8 mass each)."""
+    rng = np.random.default_rng(seed)
+    T = 3
+    parents = np.tile(np.array([-1, 0, 0], dtype=np.int32), (B, 1))
+    tl = (rng.standard_normal((B, T, V), dtype=np.float32) * 4.0).astype(np.float32)
+    tokens = np.zeros((B, T), dtype=np.int32)
+    child_logit = np.zeros((B, T), dtype=np.float32)
+    u_acc = np.zeros((B, T), dtype=np.float32)
+    for b in range(B):
+        ids = rng.choice(V, size=2 + secondary, replace=False)
+        ys, sec = ids[:2], ids[2:]
+        tokens[b, 0] = int(rng.integers(V))
+        tokens[b, 1:] = ys
+        row = synth.to_f64(synth.as_dtype(tl[b, 0], "bf16"), "bf16")
+        mx = row.max()
+        w = np.exp(row - mx)
+        w[ids] = 0.0
+        s_out = w.sum()
+        if secondary:
+            share = 9.0 / secondary                      # each secondary token: 9/k of the tail's mass
+            tl[b, 0, sec] = np.float32(mx + np.log(share * s_out))
+            s_out *= 10.0
+        # child masses: shares 0.8 and 0.2 of p_child (bf16 rounding of their logits moves them by < 7 %); the
+        # first child's q is 0.95, so both slot ratios stay below 1
+        mass = p_child / (1.0 - p_child) * s_out
+        tl[b, 0, ys[0]] = np.float32(mx + np.log(0.8 * mass))
+        tl[b, 0, ys[1]] = np.float32(mx + np.log(0.2 * mass))
+        child_logit[b, 1] = np.float32(np.log(0.95))
+        child_logit[b, 2] = np.float32(np.log(0.05))
+        u_acc[b, 1:] = np.float32(1.0 - 2.0 ** -20)     # above every acceptance ratio below 1 - 1e-6
+    u_fin = ((2 * rng.integers(0, 2 ** 23, size=B) + 1) * 2.0 ** -24).astype(np.float32)
+    cfg = synth.scaled(synth.SHAPE_7B, B=B, T=T, depth=1, V=V)
+    return dict(cfg=cfg, dtype="bf16", target_logits=synth.as_dtype(tl, "bf16"), child_logit=child_logit,
+                tokens=tokens, parents=parents, u_acc=u_acc, u_fin=u_fin, max_depth=1)
+
+
+@pytest.mark.parametrize("p_child", [0.999, 0.99999])
+def test_peaked_rows_fallback_exact(p_child):
+    inp = _peaked_inputs(64, 151936, seed=17, p_child=p_child)
+    g, o = _compare(inp)
+    assert (g["final_kind"] == 0).all() and (g["out_len"] == 1).all()
+    _compare(inp, top_p=0.95)          # the nucleus is the two children: the second is accepted
+
+
+def test_peaked_rows_nucleus_cut_outside_the_children():
+    # children 0.999 of the mass, four secondary tokens 90 % of the rest: top_p 0.9995 keeps the children and
+    # two or three secondary tokens, both children are rejected and the fallback draws among the kept ones
+    inp = _peaked_inputs(64, 151936, seed=18, p_child=0.999, secondary=4)
+    g, o = _compare(inp, top_p=0.9995)
+    assert (g["final_kind"] == 0).all()
+    _compare(inp)
+
+
 def test_deterministic():
     cfg = synth.scaled(synth.SHAPE_7B, B=32, V=8192)
     inp = synth.accept_inputs(cfg, seed=7)
