@@ -7,7 +7,7 @@ import torch
 import oracle
 import paper_2608_04962_amd as sr
 import synth
-from helpers import assert_faithful_bf16, dev_tensor, f64, row_rel_err, tol_for
+from helpers import assert_z_bf16, dev_tensor, f64, row_rel_err, z_tolerance
 
 pytestmark = pytest.mark.gpu
 
@@ -37,26 +37,27 @@ def _oracle_heads(inp, rows=None, vocab=None):
                                 round_fn=None if dt == "f32" else oracle.round_bf16)
 
 
-def _check_tree_valid(inp, tok, cl, ref_logits, rows, tol_abs):
-    """The GPU tree built from the GPU's own logits must be a valid tree under the oracle's logits: every C_u
-    is a top-m set up to the logit tolerance, siblings are distinct and child_logit is the drafted logit."""
-    cfg = inp["cfg"]
-    depth, kids = oracle.tree_structure(inp["parents"][0])
+def _check_fused_tree(inp, tok, cl, lg, rows):
+    """App. B.1 Eq. (slotq), Eq. (childlist): the tree the GPU built inside sr_heads_propose (top-m supports from
+    the vocabulary GEMM's group maxima, then the ordered draws) equals the oracle's tree build run on the
+    GPU's own fp32 head logits, bit for bit (no logit tolerance enters); only a trajectory whose draws come
+    closer than 1e-6 to a cumulative boundary may differ."""
+    rows = np.asarray(list(rows))
+    otok, ocl, mg = oracle.tree_build(lg[rows], inp["parents"][rows], inp["root_token"][rows], inp["u_tree"][rows])
+    excused = 0
     for i, b in enumerate(rows):
-        assert tok[b, 0] == inp["root_token"][b]
-        for u, ch in enumerate(kids):
-            if not ch:
-                continue
-            k = min(depth[u] + 1, cfg.H)
-            row = ref_logits[i, k - 1]
-            got = tok[b, ch]
-            assert len(set(got.tolist())) == len(ch)
-            assert (got >= 0).all() and (got < cfg.V).all()
-            ref_top = oracle.top_m(row, len(ch) + 1)
-            kth = row[ref_top[len(ch) - 1]]
-            # a chosen token may differ from the oracle's top set only within the logit tolerance
-            assert (row[got] >= kth - tol_abs).all()
-            np.testing.assert_allclose(cl[b, ch], row[got], atol=tol_abs, rtol=0)
+        if mg[i] < 1e-6:
+            excused += 1
+            continue
+        np.testing.assert_array_equal(tok[b], otok[i])
+        np.testing.assert_array_equal(cl[b], ocl[i].astype(np.float32))
+    assert excused <= max(1, len(rows) // 100), excused
+
+
+def _check_z(inp, z_rows, ref):
+    """bf16 head states: one ulp plus what the fp32 evaluation and a flipped LN rounding can move them."""
+    tol = z_tolerance(ref["x"], f64(inp["A"], inp["dtype"]))
+    assert_z_bf16(z_rows, ref["z_exact"], tol)
 
 
 def test_config0_full():
@@ -65,12 +66,7 @@ def test_config0_full():
     ref = _oracle_heads(inp)
     assert row_rel_err(z.reshape(-1, inp["cfg"].d), ref["z"].reshape(-1, inp["cfg"].d)).max() <= 1e-5
     assert row_rel_err(lg.reshape(-1, inp["cfg"].V), ref["logits"].reshape(-1, inp["cfg"].V)).max() <= 1e-5
-    _check_tree_valid(inp, tok, cl, ref["logits"], range(inp["cfg"].B), 1e-5 * np.abs(ref["logits"]).max())
-    # away from near-ties the tree is the oracle's tree
-    otok, ocl, mg = oracle.tree_build(ref["logits"], inp["parents"], inp["root_token"], inp["u_tree"])
-    for b in range(inp["cfg"].B):
-        if mg[b] > 1e-4:
-            np.testing.assert_array_equal(tok[b], otok[b])
+    _check_fused_tree(inp, tok, cl, lg, range(inp["cfg"].B))
 
 
 # B*H rows 15, 96 and 132 take the 64-, 128- and 256-row vocabulary tiles
@@ -82,24 +78,47 @@ def test_bf16_scaled(cfg_over):
     inp = synth.heads_inputs(cfg, seed=1)
     tok, cl, lg, z = _gpu_heads(inp)
     ref = _oracle_heads(inp)
-    assert_faithful_bf16(z, ref["z_exact"])
+    _check_z(inp, z, ref)
     lerr = row_rel_err(lg.reshape(-1, cfg.V), ref["logits"].reshape(-1, cfg.V))
     assert lerr.max() <= 2e-3, lerr.max()
-    _check_tree_valid(inp, tok, cl, ref["logits"], range(cfg.B), 2e-3 * np.abs(ref["logits"]).max())
+    _check_fused_tree(inp, tok, cl, lg, range(cfg.B))
+
+
+def _full_size(cfg, rows, tree_rows):
+    print(f"[heads] {cfg.name} B={cfg.B} T={cfg.T}", flush=True)
+    inp = synth.heads_inputs(cfg, seed=0)
+    tok, cl, lg, z = _gpu_heads(inp)
+    ref = _oracle_heads(inp, rows=rows)
+    _check_z(inp, z[rows], ref)
+    lerr = row_rel_err(lg[rows].reshape(-1, cfg.V), ref["logits"].reshape(-1, cfg.V))
+    assert lerr.max() <= 2e-3, lerr.max()
+    _check_fused_tree(inp, tok, cl, lg, tree_rows)
+    return inp
 
 
 @pytest.mark.parametrize("name,rseed", [("1.5B-shape", 1), ("7B-shape", 2), ("14B-shape-tail", 3)])
 def test_full_size_sampled(name, rseed):
     cfg = synth.WORKLOADS[name]
-    print(f"[heads] {cfg.name}", flush=True)
-    inp = synth.heads_inputs(cfg, seed=0)
-    tok, cl, lg, z = _gpu_heads(inp)
-    rows = np.random.default_rng(rseed).choice(cfg.B, size=min(3, cfg.B), replace=False)
-    ref = _oracle_heads(inp, rows=rows)
-    assert_faithful_bf16(z[rows], ref["z_exact"])
-    lerr = row_rel_err(lg[rows].reshape(-1, cfg.V), ref["logits"].reshape(-1, cfg.V))
-    assert lerr.max() <= 2e-3, lerr.max()
-    _check_tree_valid(inp, tok, cl, ref["logits"], rows, 2e-3 * np.abs(ref["logits"]).max())
+    rng = np.random.default_rng(rseed)
+    rows = rng.choice(cfg.B, size=min(3, cfg.B), replace=False)
+    _full_size(cfg, rows, rng.choice(cfg.B, size=min(12, cfg.B), replace=False))
+
+
+@pytest.mark.parametrize("point", synth.SWEEP_POINTS, ids=lambda p: f"B{p[0]}-T{p[1]}")
+def test_sweep_points_sampled(point):
+    # the concurrency sweep at full size: B*H from 1024 rows (four 256-row vocabulary tiles) down to 16, Reflex
+    # corrections on a random half of the trajectories; sampled rows include both kinds and the last row
+    cfg = synth.sweep_config(*point)
+    act = synth.heads_inputs(cfg, seed=0, with_weights=False)["active"].astype(bool)
+    rng = np.random.default_rng(point[0] * 1000 + point[1])
+    on, off = np.flatnonzero(act), np.flatnonzero(~act)
+    rows = [cfg.B - 1]
+    for grp in (on, off):
+        if len(grp):
+            rows += list(rng.choice(grp, size=min(2, len(grp)), replace=False))
+    rows = np.unique(np.asarray(rows))
+    assert act[rows].any() and (~act[rows]).any()
+    _full_size(cfg, rows, rng.choice(cfg.B, size=min(8, cfg.B), replace=False))
 
 
 # ---------------------------------------------------------------- tree build alone: bit-exact

@@ -203,7 +203,7 @@ def _gpu_heads_reflex(inp, gin, P=True):
 
 @pytest.mark.parametrize("name,over", [("tiny-fp32", None), ("1.5B-shape", dict(B=5, V=20000))])
 def test_gated_correction_parity(name, over):
-    from helpers import assert_faithful_bf16, f64
+    from helpers import assert_z_bf16, bf16_ulp, f64, z_tolerance
     cfg = synth.TINY_FP32 if over is None else synth.scaled(synth.SHAPE_1P5B, **over)
     inp = synth.heads_inputs(cfg, seed=7)
     gin = synth.reflex_gate_inputs(cfg, seed=7)
@@ -214,6 +214,9 @@ def test_gated_correction_parity(name, over):
                                f64(inp["bias"], dt), f64(inp["W"], dt), cfg.clip_norm, 1e-5,
                                round_fn=None if dt == "f32" else oracle.round_bf16)
     W64 = f64(inp["W"], dt)
+    # the corrected state inherits the head state's deviation (one ulp plus the flipped-LN bound) on top of
+    # its own rounding
+    zin_tol = None if dt == "f32" else bf16_ulp(ref["z_exact"]) + z_tolerance(ref["x"], f64(inp["A"], dt))
     opened = 0
     for b in range(cfg.B):
         for h in range(cfg.H):
@@ -230,7 +233,7 @@ def test_gated_correction_parity(name, over):
                 assert row_rel_err(z[b, h], zt) <= 1e-5
                 zr = zt
             else:
-                assert_faithful_bf16(z[b, h][None], zt[None])
+                assert_z_bf16(z[b, h][None], zt[None], zin_tol[b, h][None])
                 zr = oracle.round_bf16(zt)
             assert row_rel_err(lg[b, h], W64 @ zr) <= (1e-5 if dt == "f32" else 2e-3)
     assert 0 < opened < cfg.B * cfg.H
