@@ -703,12 +703,14 @@ __device__ __forceinline__ void attn_item_dma(
   auto issue = [&](int i, unsigned char* slot) __attribute__((always_inline)) { issue_prod(i, slot); };
   // V of a tile, bf16 -> fp16 in place: every converting lane takes whole 16-byte chunks (their positions
   // do not matter). The reads (conv_load) are issued early and the converted chunks written later
-  // (conv_store), so the LDS latency overlaps other work. The conversion is exact for a zero and for
-  // magnitudes in [2^-14, 65280] (bf16 patterns 0x3880..0x477f without the sign); each converting lane
-  // keeps the largest magnitude pattern and the smallest nonzero one (minus one, so zero wraps to 0xffff)
-  // of everything it converts, two 16-bit lanes per register.
+  // (conv_store), so the LDS latency overlaps other work. The conversion is exact for magnitudes in
+  // [2^-14, 65280] and rounds smaller ones to fp16's subnormal step, an absolute error of at most 2^-25;
+  // larger ones would overflow. Each converting lane keeps the largest magnitude pattern of everything it
+  // converts (two 16-bit lanes per register): an item is recomputed with fp32 V when that exceeds 65280
+  // (pattern 0x477f; inf and NaN included) or when the item's largest |v| is below 2^-6 (pattern 0x3c80),
+  // where 2^-25 would no longer be negligible against the scale of V.
   u32x4 cw[G::CPL];
-  u16x2 vmag_hi = {0, 0}, vmag_lo = {0xffff, 0xffff};
+  u16x2 vmag_hi = {0, 0};
   auto conv_load = [&](const unsigned char* v) __attribute__((always_inline)) {
     if (tr_rank < 0) return;                    // the DMA wave
     int ln = lane;
@@ -733,11 +735,8 @@ __device__ __forceinline__ void attn_item_dma(
           h[e] = (_Float16)bf2f((e & 1) ? (cw[k][e >> 1] >> 16) : (cw[k][e >> 1] & 0xffffu));
         *(f16x8*)(v + it * 16) = h;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const u16x2 mag = __builtin_bit_cast(u16x2, cw[k][w] & 0x7fff7fffu);
-          vmag_hi = __builtin_elementwise_max(vmag_hi, mag);
-          vmag_lo = __builtin_elementwise_min(vmag_lo, mag - (u16x2){1, 1});
-        }
+        for (int w = 0; w < 4; ++w)
+          vmag_hi = __builtin_elementwise_max(vmag_hi, __builtin_bit_cast(u16x2, cw[k][w] & 0x7fff7fffu));
       }
     }
   };
@@ -909,14 +908,15 @@ __device__ __forceinline__ void attn_item_dma(
     }
   }
 
-  // ---- a V value outside fp16's exact range: list the item for the fp32-V recomputation (its outputs
-  // written below are then overwritten before anything reads them)
+  // ---- V too large for fp16 or too small for its subnormal step: list the item for the fp32-V
+  // recomputation (its outputs written below are then overwritten before anything reads them). Items
+  // without tiles (invalid input) are not listed.
   {
-    const uint32_t hi = max((uint32_t)vmag_hi[0], (uint32_t)vmag_hi[1]);
-    const uint32_t lo = min((uint32_t)vmag_lo[0], (uint32_t)vmag_lo[1]);
-    if (__ballot(hi > 0x477fu || lo < 0x387fu) != 0 && lane == 0) atomicOr(&meta.vwide, 1);
+    uint32_t hi = max((uint32_t)vmag_hi[0], (uint32_t)vmag_hi[1]);
+    hi = (uint32_t)warp_max_i((int)hi);
+    if (tr_rank >= 0 && lane == 0) atomicMax(&meta.vwide, (int)hi);
     __syncthreads();
-    if (threadIdx.x == 0 && meta.vwide != 0) {
+    if (threadIdx.x == 0 && n_tiles > 0 && (meta.vwide > 0x477f || meta.vwide < 0x3c80)) {
       const unsigned k = atomicAdd(redo, 1u);
       redo[1 + k] = (unsigned)item;
     }

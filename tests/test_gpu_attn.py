@@ -154,9 +154,10 @@ def _scale_values(inp, traj, fn):
 
 
 def test_bf16_v_outside_fp16_range():
-    """bf16 V values that fp16 cannot hold exactly: magnitudes around 1e5 (beyond fp16's 65504), around
-    1e-6 (below its normal range), around 1e-30 and a mix of huge and tiny values in one trajectory. The
-    items holding them are recomputed with fp32 V; every trajectory matches the oracle."""
+    """bf16 V beyond what the fp16 product keeps: magnitudes around 1e5 (fp16 overflows past 65504), V scaled to
+    around 1e-6 and 1e-30 (below fp16's normal range, so its subnormal step would dominate) and a mix of huge
+    and tiny values in one trajectory. Those items are recomputed with fp32 V; the others (N(0,1) values, a
+    few of them below 2^-14) keep the fp16 product; every trajectory matches the oracle."""
     cfg = synth.scaled(synth.SHAPE_7B, B=6, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 300, 2600))
     inp = synth.attn_inputs(cfg, seed=12)
     inp = _scale_values(inp, 1, lambda v: v * 1.0e5)
