@@ -203,6 +203,29 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
                               float* out, float* lse,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * sr_tree_verify_attn without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc). Arguments and results as sr_tree_verify_attn. The
+ * scratch the call needs (the chunk partials, the work-item counter and the
+ * fp32-V recomputation list: sr_tree_verify_attn_workspace bytes) lives in a
+ * static device array of SR_ATTN_NOALLOC_MAX_BYTES per GPU, which the library
+ * holds on every GPU it runs on until the process ends; the call itself
+ * allocates nothing. A request that needs more returns SR_ERR_UNSUPPORTED with
+ * nothing enqueued (use sr_tree_verify_attn with a workspace instead). The
+ * current device must be the stream's device. Every call on one GPU shares
+ * that GPU's array and leaves its contents there; the counters are zeroed by a
+ * kernel on the stream at each call (no memset), so calls ordered on one stream
+ * are safe, while calls that overlap on one GPU (other streams or threads
+ * without ordering) race and give wrong results.
+ */
+#define SR_ATTN_NOALLOC_MAX_BYTES (256u << 20)
+sr_status sr_tree_verify_attn_noalloc(const sr_attn_desc* desc,
+                                      const void* q, const void* k_cache, const void* v_cache,
+                                      const int32_t* block_table, const int32_t* ctx_len,
+                                      const void* k_tree, const void* v_tree, const int32_t* parents,
+                                      float* out, float* lse, void* stream);
+
 /* ========================================================================== *
  * 3. Exact acceptance walk (App. B.2)
  * ========================================================================== *

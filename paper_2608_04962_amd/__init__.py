@@ -28,7 +28,7 @@ from . import _lib
 from ._lib import (AcceptDesc, AttnDesc, BudgetDesc, CommitDesc, HeadsDesc, ReflexDesc, ReflexGateDesc,  # noqa: F401
                    SpecRollError, check, lib)
 
-__all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_accept", "commit_path", "tree_budget",
+__all__ = ["heads_propose", "tree_build", "tree_verify_attn", "tree_verify_attn_noalloc", "tree_accept", "commit_path", "tree_budget",
            "reflex_feedback", "heads_propose_reflex", "prof_begin", "prof_end",
            "kernel_names", "version", "SpecRollError", "library_path"]
 
@@ -190,6 +190,37 @@ def tree_verify_attn(q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, 
                                    _ptr(ctx_len), _ptr(k_tree), _ptr(v_tree), _ptr(parents), _ptr(out),
                                    _ptr(lse), _ptr(ws), wsb, _stream(dev))
     check(st, "sr_tree_verify_attn")
+    return out, lse
+
+
+def tree_verify_attn_noalloc(q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, scale=None,
+                             out=None, lse=None, want_lse: bool = True):
+    """tree_verify_attn through sr_tree_verify_attn_noalloc: no workspace; the library's per-GPU scratch array
+    holds the partial results (calls overlapping on one GPU race). Outputs as tree_verify_attn."""
+    dev = q.device
+    B, T, Hq, D = q.shape
+    NB, Hkv, bs, _ = k_cache.shape
+    dt = q.dtype
+    _need(q, "q", None, (B, T, Hq, D), dev)
+    if dt not in _DT:
+        raise TypeError("q must be float32 or bfloat16")
+    _need(k_cache, "k_cache", dt, (NB, Hkv, bs, D), dev)
+    _need(v_cache, "v_cache", dt, (NB, Hkv, bs, D), dev)
+    _need(block_table, "block_table", torch.int32, (B, block_table.shape[1]), dev)
+    _need(ctx_len, "ctx_len", torch.int32, (B,), dev)
+    _need(k_tree, "k_tree", dt, (B, T, Hkv, D), dev)
+    _need(v_tree, "v_tree", dt, (B, T, Hkv, D), dev)
+    _need(parents, "parents", torch.int32, (B, T), dev)
+    out = torch.empty((B, T, Hq, D), dtype=torch.float32, device=dev) if out is None else out
+    _need(out, "out", torch.float32, (B, T, Hq, D), dev)
+    if want_lse and lse is None:
+        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=dev)
+    desc = attn_desc(q, k_cache, block_table, scale)
+    with torch.cuda.device(dev):
+        st = lib().sr_tree_verify_attn_noalloc(C.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                               _ptr(block_table), _ptr(ctx_len), _ptr(k_tree), _ptr(v_tree),
+                                               _ptr(parents), _ptr(out), _ptr(lse), _stream(dev))
+    check(st, "sr_tree_verify_attn_noalloc")
     return out, lse
 
 

@@ -74,6 +74,7 @@ SIGNATURES = {
     "sr_tree_verify_attn_workspace": (C.c_size_t, [C.POINTER(AttnDesc)]),
     "sr_tree_verify_attn": (C.c_int, [C.POINTER(AttnDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                       C.c_size_t, _p]),
+    "sr_tree_verify_attn_noalloc": (C.c_int, [C.POINTER(AttnDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]),
     "sr_tree_accept_workspace": (C.c_size_t, [C.POINTER(AcceptDesc)]),
     "sr_tree_accept": (C.c_int, [C.POINTER(AcceptDesc), _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                  C.c_size_t, _p]),

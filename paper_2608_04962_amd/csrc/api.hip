@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -131,6 +132,40 @@ static sr_status check_ws(const void* ws, size_t have, size_t need) {
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ---------------------------------------------------------------- scratch of the allocation-free attention call
+// One array per GPU, created with the library's code object on that GPU and held until the process ends. In
+// host code `scratch` names a host-side stand-in, never the device memory: its device address is taken once
+// per device with hipGetSymbolAddress and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[SR_ATTN_NOALLOC_MAX_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+// device address of the current device's scratch array (looked up at the first call on that device)
+static sr_status scratch_base(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("device %d: at most %d devices are supported", dev, kMaxDevices);
+    return SR_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr || ((uintptr_t)p & 255u) != 0) {
+      set_error("scratch array of device %d has no usable device address", dev);
+      return SR_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SR_OK;
+}
 
 }  // namespace sr
 
@@ -315,6 +350,26 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* d, const void* q, const void* 
   if (st != SR_OK) return st;
   return run_attn(d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse,
                   (char*)workspace, stream);
+}
+
+sr_status sr_tree_verify_attn_noalloc(const sr_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
+                                      const int32_t* block_table, const int32_t* ctx_len, const void* k_tree,
+                                      const void* v_tree, const int32_t* parents, float* out, float* lse,
+                                      void* stream) {
+  sr_status st = check_attn_args(d, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out);
+  if (st != SR_OK) return st;
+  const AttnPlan p = attn_plan(*d);
+  const size_t need = align_up(p.part_o_bytes) + align_up(p.part_ml_bytes) + align_up(p.work_bytes);
+  if (need > (size_t)SR_ATTN_NOALLOC_MAX_BYTES) {
+    set_error("request needs %zu bytes of scratch; the allocation-free call holds %zu "
+              "(use sr_tree_verify_attn with a workspace)", need, (size_t)SR_ATTN_NOALLOC_MAX_BYTES);
+    return SR_ERR_UNSUPPORTED;
+  }
+  void* base = nullptr;
+  st = scratch_base(&base);
+  if (st != SR_OK) return st;
+  return run_attn(d, p, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out, lse, (char*)base,
+                  stream);
 }
 
 // ------------------------------------------------------------------ acceptance
