@@ -74,8 +74,8 @@ def algorithmic(cfg, ctx_len, kernel):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=32, help="trajectories the oracle runs on")
@@ -193,6 +193,43 @@ def main():
     assert (kinds != 255).all(), "invalid trajectories in the benchmark step"
     assert torch.isfinite(out).all().item()
 
+    # MALL (256 MB last-level cache) check: the same step with 1 GiB written between steps (outside each
+    # step's event pair) against the back-to-back steps above
+    flush = torch.empty(CALIB_ELEMS, dtype=torch.float32, device=dev)
+    fl_ms = []
+    for _ in range(20):
+        flush.fill_(1.0)
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record()
+        step()
+        f1.record()
+        torch.cuda.synchronize()
+        fl_ms.append(f0.elapsed_time(f1))
+    del flush
+    torch.cuda.empty_cache()
+    mall = {"flushed_step_ms_p50": float(np.median(fl_ms)), "back_to_back_step_ms_p50": float(np.percentile(per_step, 50)),
+            "flush_bytes": CALIB_ELEMS * 4, "steps": len(fl_ms)}
+    mall["ratio"] = mall["flushed_step_ms_p50"] / mall["back_to_back_step_ms_p50"]
+
+    # acceptance walk alone: algorithmic bytes = one target row per visited node (out_len rows per trajectory)
+    sr.prof_begin("sr_tree_accept")
+    for _ in range(20):
+        sr.tree_accept(C_["target_logits"], C_["child_logit"], C_["tokens"], C_["parents"], C_["u_acc"],
+                       C_["u_fin"], md, outputs=outs)
+    acc_ms, acc_n = sr.prof_end()
+    acc_avg = acc_ms / max(acc_n, 1)
+    rows_read = int(outs["out_len"].sum().item())
+    acc_bytes = rows_read * cfg.V * 2 + B * T * 16
+    vocab = algorithmic(cfg, ain["ctx_len"], "sr_vocab_gemm")
+    headg = algorithmic(cfg, ain["ctx_len"], "sr_head_gemm")
+    gemms = {}
+    for kname, a in (("sr_vocab_gemm", vocab), ("sr_head_gemm", headg)):
+        kms = per_kernel.get(kname, float("nan"))
+        gemms[kname] = {"ms": kms, "TFLOP/s": a["flops"] / (kms / 1e3) / 1e12,
+                        "frac_bf16_peak": a["flops"] / (kms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+                        "GB/s": a["bytes"] / (kms / 1e3) / 1e9,
+                        "frac_hbm_peak": a["bytes"] / (kms / 1e3) / 1e9 / HBM_PEAK_GBPS}
+
     res = {
         "metric": METRIC, "value": value, "unit": "tree tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
@@ -206,6 +243,11 @@ def main():
         "step_ms": {"p50": float(np.percentile(per_step, 50)), "p90": float(np.percentile(per_step, 90)),
                     "min": float(per_step[0]), "max": float(per_step[-1])},
         "tree_attn": {"GB/s": attn_gbps, "frac_hbm_peak": attn_gbps / HBM_PEAK_GBPS, "ms": attn_ms},
+        "tree_accept": {"avg_ms": acc_avg, "launches": acc_n, "rows_read": rows_read, "algorithmic_bytes": acc_bytes,
+                        "GB/s": acc_bytes / (acc_avg / 1e3) / 1e9,
+                        "frac_hbm_peak": acc_bytes / (acc_avg / 1e3) / 1e9 / HBM_PEAK_GBPS},
+        "head_gemms": gemms,
+        "mall_check": mall,
         "kernels_ms": per_kernel,
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
     }
@@ -473,25 +515,33 @@ def measured_traffic(kernel):
         return None
 
 
-def cpu_baseline(cfg, hin, ain, cin, k):
-    """The float64 oracle on the first k trajectories of the same workload, on the host cores."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def oracle_step(cfg, hin, ain, cin, rows):
+    """Seconds the float64 oracle takes for the step on trajectories ``rows``: (heads + tree, attention of every
+    node, acceptance)."""
     import numpy as np
 
     import oracle
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
     dt = cfg.dtype
-    rows = np.arange(k)
-    f = lambda x: synth.to_f64(x, dt)
+    f = lambda x: synth.to_f64(x, dt)  # noqa: E731
+    rows = np.asarray(rows)
     A64, b64, W64 = f(hin["A"]), f(hin["bias"]), f(hin["W"])
     q, kc, vc, kt, vt = (f(ain[n]) for n in ("q", "k_cache", "v_cache", "k_tree", "v_tree"))
     t0 = time.perf_counter()
     ho = oracle.heads_forward(f(hin["hidden"])[rows], hin["corr"][rows], hin["active"][rows], A64, b64, W64,
-                              cfg.clip_norm, 1e-5, round_fn=oracle.round_bf16)
+                              cfg.clip_norm, 1e-5, round_fn=None if dt == "f32" else oracle.round_bf16)
     oracle.tree_build(ho["logits"], hin["parents"][rows], hin["root_token"][rows], hin["u_tree"][rows])
     t1 = time.perf_counter()
     oracle.tree_attention(q, kc, vc, ain["block_table"], ain["ctx_len"], kt, vt, ain["parents"], ain["scale"],
@@ -504,11 +554,39 @@ def cpu_baseline(cfg, hin, ain, cin, k):
     oracle.tree_accept(Rows(), cin["child_logit"], cin["tokens"], cin["parents"], cin["u_acc"], cin["u_fin"], 1.0,
                        cin["max_depth"], rows=[int(b) for b in rows])
     t3 = time.perf_counter()
-    secs = t3 - t0
-    return {"value": k * cfg.T / secs, "unit": "tree tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{k} of {cfg.B} trajectories of the same workload (all {cfg.T} nodes each): heads+tree "
-                      f"{t1 - t0:.1f}s, attention {t2 - t1:.1f}s, acceptance {t3 - t2:.1f}s; float64 NumPy",
-            "seconds": secs}
+    return t1 - t0, t2 - t1, t3 - t2
+
+
+def cpu_baseline(cfg, hin, ain, cin, k):
+    """The float64 oracle on the first k trajectories of the same workload on the host cores (BLAS threads as the
+    process has them), plus single-thread figures of the tiny fp32 workload (whole) and of the 1.5B-shaped one
+    (two trajectories)."""
+    import synth
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threadpool_limits = None
+        threads = len(os.sched_getaffinity(0))
+    th, ta, tc = oracle_step(cfg, hin, ain, cin, range(k))
+    secs = th + ta + tc
+    res = {"value": k * cfg.T / secs, "unit": "tree tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"{k} of {cfg.B} trajectories of the same workload (all {cfg.T} nodes each): heads+tree "
+                     f"{th:.1f}s, attention {ta:.1f}s, acceptance {tc:.1f}s; float64 NumPy",
+           "seconds": secs, "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0))}
+    single = {}
+    if threadpool_limits is not None:
+        for c, n in ((synth.TINY_FP32, synth.TINY_FP32.B), (synth.SHAPE_1P5B, 2)):
+            h = synth.heads_inputs(c, seed=0)
+            a = synth.attn_inputs(c, seed=0)
+            ac = synth.accept_inputs(c, seed=0)
+            with threadpool_limits(limits=1):
+                t = oracle_step(c, h, a, ac, range(n))
+            single[c.name] = {"tree_tokens_per_s": n * c.T / sum(t), "trajectories": n, "seconds": sum(t),
+                              "heads_tree_s": t[0], "attention_s": t[1], "acceptance_s": t[2]}
+            del h, a, ac
+    res["single_thread"] = single
+    return res
 
 
 if __name__ == "__main__":
