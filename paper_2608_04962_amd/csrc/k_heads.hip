@@ -6,6 +6,8 @@
 // logits through the target's vocabulary projection); App. B.1 Eq. (slotq), Eq. (childlist).
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "select.hpp"
@@ -282,6 +284,51 @@ template <int CPR> __device__ __forceinline__ int gemm_swz(int r) {
   return (r >> SH) & (CPR - 1);
 }
 
+// Output of a transposed accumulator block (lane owns row m0w + 32 i + l%32; register r of tile j holds
+// column n0w + 32 j + 8 (r/4) + 4 (l/32) + r%4): the 64-column group maxima, then the logits. Stored straight
+// from registers, each 16-byte store instruction would touch 64 rows (64 cache lines); instead the wave stages
+// its 32 rows of one tile row in its own LDS area stg (32 rows of WTN*4 + 16 bytes: the padding puts the 16
+// lanes of a quarter-wave on 16 distinct bank groups) and stores them back with WTN/4 consecutive lanes per
+// row. One wave; the caller makes sure no other wave still reads stg.
+template <int TM, int TN, int WTN, class Epi>
+__device__ __forceinline__ void epi_trans(const f32x16 (&acc)[TM][TN], unsigned char* stg, int m0w, int n0w, int M,
+                                          int N, const Epi& epi) {
+  static_assert(!Epi::kGroupMax || WTN % 64 == 0, "whole 64-column groups per wave");
+  constexpr int RS = WTN * 4 + 16;              // staged row stride in bytes
+  constexpr int LPR = WTN / 4;                  // lanes per staged row on the way out
+  static_assert(64 % LPR == 0, "whole rows per store instruction");
+  const int lane = threadIdx.x & 63, fr = lane & 31, fh = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int mb = m0w + i * 32, m = mb + fr;
+#pragma unroll
+    for (int g = 0; g < (TN + 1) / 2; ++g) {   // 64-column group g of this wave: tiles 2g, 2g+1
+      float gm = -INFINITY;
+#pragma unroll
+      for (int j = 2 * g; j < 2 * g + 2 && j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = j * 32 + 8 * q + 4 * fh;
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          *(f32x4*)(stg + fr * RS + c * 4) = v;
+          if (n0w + c < N) gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+        }
+      if constexpr (Epi::kGroupMax) {
+        gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
+        if (fh == 0 && m < M) epi.group_max(m, n0w / 64 + g, gm);
+      }
+    }
+    // this wave's own LDS writes above precede its reads below (one wave, in order)
+#pragma unroll
+    for (int rr = 0; rr < 32; rr += 64 / LPR) {
+      const int row = rr + lane / LPR, c = (lane % LPR) * 4;
+      const f32x4 v = *(const f32x4*)(stg + row * RS + c * 4);
+      const int n = n0w + c;
+      if (mb + row < M && n < N) epi.store4(mb + row, n, v);
+    }
+  }
+}
+
 template <int BM, int BN, int BK, int WGM, int WGN, int STAGES, class Epi>
 __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __restrict__ A,
                                                             const bf16_t* __restrict__ B, int M, int N, int K,
@@ -404,47 +451,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
   }
 
   if constexpr (Epi::kTrans) {
-    // lane owns row m = .. + l%32; register r of tile j holds column 32*j + 8*(r/4) + 4*(l/32) + r%4.
-    // Stored straight from registers, each 16-byte store instruction would touch 64 rows (64 cache
-    // lines); instead each wave stages its 32 rows of one tile row through its own part of the ring
-    // (rows padded by 16 bytes: the 16 lanes of a quarter-wave write 16 distinct bank groups) and
-    // stores them back with WTN/4 consecutive lanes per row.
-    static_assert(!Epi::kGroupMax || WTN % 64 == 0, "whole 64-column groups per wave");
-    constexpr int RS = WTN * 4 + 16;              // staged row stride in bytes
-    constexpr int LPR = WTN / 4;                  // lanes per staged row on the way out
-    static_assert(64 % LPR == 0, "whole rows per store instruction");
-    static_assert(NW * 32 * RS <= STAGES * (A_BYTES + B_BYTES), "staging fits the ring");
+    static_assert(NW * 32 * (WTN * 4 + 16) <= STAGES * (A_BYTES + B_BYTES), "staging fits the ring");
     __syncthreads();                              // every wave has read its last fragments from the ring
-    unsigned char* stg = &lds[0][0] + wave * 32 * RS;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int mb = m0 + wm * WTM + i * 32, m = mb + fr;
-#pragma unroll
-      for (int g = 0; g < (TN + 1) / 2; ++g) {   // 64-column group g of this wave: tiles 2g, 2g+1
-        float gm = -INFINITY;
-#pragma unroll
-        for (int j = 2 * g; j < 2 * g + 2 && j < TN; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int c = j * 32 + 8 * q + 4 * fh;
-            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-            *(f32x4*)(stg + fr * RS + c * 4) = v;
-            if (n0 + wn * WTN + c < N) gm = fmaxf(gm, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-          }
-        if constexpr (Epi::kGroupMax) {
-          gm = fmaxf(gm, __shfl_xor(gm, 32, 64));
-          if (fh == 0 && m < M) epi.group_max(m, (n0 + wn * WTN) / 64 + g, gm);
-        }
-      }
-      // this wave's own LDS writes above precede its reads below (one wave, in order)
-#pragma unroll
-      for (int rr = 0; rr < 32; rr += 64 / LPR) {
-        const int row = rr + lane / LPR, c = (lane % LPR) * 4;
-        const f32x4 v = *(const f32x4*)(stg + row * RS + c * 4);
-        const int n = n0 + wn * WTN + c;
-        if (mb + row < M && n < N) epi.store4(mb + row, n, v);
-      }
-    }
+    epi_trans<TM, TN, WTN>(acc, &lds[0][0] + wave * 32 * (WTN * 4 + 16), m0 + wm * WTM, n0 + wn * WTN, M, N, epi);
   } else {
     // element stores (lane column l%32, register r -> row 8*(r/4) + 4*(l/32) + r%4)
 #pragma unroll
@@ -459,6 +468,160 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_dl(const bf16_t* __rest
         }
       }
   }
+}
+
+// ============================================================================ bf16 GEMM, quarter tiles
+// C^T tiles of 256 x 256 for the vocabulary projection (M = B*H > 128), four waves in 2 x 2, each owning a
+// 128 x 128 quarter as 4 x 4 MFMA tiles of 32 x 32: half the LDS operand reads per MFMA of the 128 x 64
+// quarters of eight waves, with the 256 accumulator registers of a wave in AGPRs (one wave per SIMD). The
+// operands stream into a STAGES-deep ring of 32-element K-steps (direct-to-LDS, as k_gemm_dl); the fragments
+// of one 16-deep K-slice are read while the MFMAs of the previous slice run, and each wave's eight DMA
+// transfers per step are spread one per four MFMAs over two slices. One barrier per K-step, between its two
+// slices. Per-phase cycle counts (s_memtime) of a 7B-shaped run: 719 cycles for the first slice, 79 at the
+// barrier, 599 for the second, against 512 per slice of MFMA work; issued back to back after the barrier the
+// transfers had cost ~600 cycles per step.
+// ring depth of the quarter-tile GEMM: 4 (128 KB) measured within 2 % of 3 and 5 at the 7B shape
+#ifndef SR_GQ_STAGES
+#define SR_GQ_STAGES 4
+#endif
+template <int STAGES, class Epi>
+__global__ __launch_bounds__(256, 1) void k_gemm_q(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, int M,
+                                                   int N, int K, int tiles_m, int tiles_n, Epi epi) {
+  static_assert(Epi::kTrans, "transposed accumulators (lane <-> row)");
+  constexpr int BM = 256, BN = 256, BK = 32, NW = 4, WT = 128, T4 = 4;
+  constexpr int ROWB = BK * 2, CPR = ROWB / 16, RPB = 1024 / ROWB;   // 64-byte rows, 4 chunks, 16 rows per KB
+  constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB, SLOT = A_BYTES + B_BYTES;
+  constexpr int A_BLK = A_BYTES / 1024, B_BLK = B_BYTES / 1024;
+  constexpr int DPW = (A_BLK + B_BLK) / NW;      // DMA instructions per wave per K-step
+  static_assert((STAGES - 2) * DPW <= 63 && STAGES >= 3, "stages in flight fit the vmcnt counter");
+  static_assert(NW * 32 * (WT * 4 + 16) <= STAGES * SLOT, "epilogue staging fits the ring");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES][SLOT];
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int fr = lane & 31, fh = lane >> 5;
+  // XCD-aware block -> (mt, nt): the M tiles of one N tile run on one XCD at the same time
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int mt = local % tiles_m, nt = (local / tiles_m) * 8 + xcd;
+  if (nt >= tiles_n) return;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int nk = K / BK;
+
+  // per-lane 32-bit source offsets of this wave's DMA blocks (rows past M or N re-read the last row)
+  uint32_t offA[A_BLK / NW], offB[B_BLK / NW];
+#pragma unroll
+  for (int j = 0; j < A_BLK / NW; ++j) {
+    const int r = (wave + j * NW) * RPB + lane / CPR, c = (lane % CPR) ^ gemm_swz<CPR>(r);
+    offA[j] = (uint32_t)min(m0 + r, M - 1) * (uint32_t)K * 2u + c * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < B_BLK / NW; ++j) {
+    const int r = (wave + j * NW) * RPB + lane / CPR, c = (lane % CPR) ^ gemm_swz<CPR>(r);
+    offB[j] = (uint32_t)min(n0 + r, N - 1) * (uint32_t)K * 2u + c * 16;
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)&lds[0][0];
+  // transfer q (0..DPW-1) of this wave for step ks: A blocks first, then B blocks
+  auto issue_one = [&](int ks, int q) __attribute__((always_inline)) {
+    const uint32_t dst = lds0 + (uint32_t)(ks % STAGES) * SLOT;
+    const uint32_t koff = (uint32_t)ks * ROWB;
+    if (q < A_BLK / NW) lds_dma16_sv(offA[q] + koff, A, dst + (wave + q * NW) * 1024);
+    else lds_dma16_sv(offB[q - A_BLK / NW] + koff, B, dst + A_BYTES + (wave + (q - A_BLK / NW) * NW) * 1024);
+  };
+  auto issue = [&](int ks) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < DPW; ++q) issue_one(ks, q);
+  };
+
+  // fragment of 32 rows x 16 K for row block rb (0..7 over the tile: A rows 32 rb, or B rows 32 (rb - 4)...):
+  // lane reads row 32 i + l%32 at chunk 2 kk + l/32 (swizzled; the swizzle depends on l%32 only)
+  const int sw = gemm_swz<CPR>(fr);
+  const uint32_t a_off[2] = {(uint32_t)((wm * WT + fr) * ROWB + ((0 + fh) ^ sw) * 16),
+                             (uint32_t)((wm * WT + fr) * ROWB + ((2 + fh) ^ sw) * 16)};
+  const uint32_t b_off[2] = {(uint32_t)(A_BYTES + (wn * WT + fr) * ROWB + ((0 + fh) ^ sw) * 16),
+                             (uint32_t)(A_BYTES + (wn * WT + fr) * ROWB + ((2 + fh) ^ sw) * 16)};
+  struct Frag { u32x4 a[T4], b[T4]; };
+  auto read_a = [&](int ks, int kk, int i) __attribute__((always_inline)) -> u32x4 {
+    return *(const u32x4*)(&lds[ks % STAGES][0] + a_off[kk] + i * 32 * ROWB);
+  };
+  auto read_b = [&](int ks, int kk, int j) __attribute__((always_inline)) -> u32x4 {
+    return *(const u32x4*)(&lds[ks % STAGES][0] + b_off[kk] + j * 32 * ROWB);
+  };
+
+  f32x16 acc[T4][T4];
+#pragma unroll
+  for (int i = 0; i < T4; ++i)
+#pragma unroll
+    for (int j = 0; j < T4; ++j) acc[i][j] = (f32x16){};
+
+  // 16 MFMAs of one slice (fragments f, tile (i, j) at step 4 i + j), with the eight reads of the next slice
+  // (ks2, kk2) into g issued after the first eight, in the order the next slice first uses them (b0, a0, b1,
+  // b2, b3, a1, a2, a3): every read has at least eight MFMAs to land. dma = 1 or 2: the first or second half of
+  // the DMA transfers of step kd, one after every fourth MFMA (issued back to back right after the barrier by
+  // all four waves, the transfers queued at the CU's address unit for ~600 cycles per step while no MFMA ran).
+  auto slice = [&](const Frag& f, Frag& g, auto more, auto dma, int ks2, int kk2, int kd) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < T4 * T4; ++t) {
+      const int i = t / T4, j = t % T4;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.b[j]),
+                                                          __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j], 0, 0, 0);
+      if (decltype(more)::value && t < 2 * T4) {
+        if (t == 0) g.b[0] = read_b(ks2, kk2, 0);
+        else if (t == 1) g.a[0] = read_a(ks2, kk2, 0);
+        else if (t < 5) g.b[t - 1] = read_b(ks2, kk2, t - 1);
+        else g.a[t - 4] = read_a(ks2, kk2, t - 4);
+      }
+      if (decltype(dma)::value != 0 && (t % 4) == 3) issue_one(kd, (decltype(dma)::value - 1) * (DPW / 2) + t / 4);
+      __builtin_amdgcn_sched_barrier(0);        // keep the MFMA / read / DMA order as written
+    }
+  };
+  static_assert(DPW == 8, "half a step's transfers per slice, one per four MFMAs");
+
+#pragma unroll
+  for (int t = 0; t < STAGES; ++t)
+    if (t < nk) issue(t);
+  dma_stage_sync<DPW, STAGES - 1>(min(STAGES - 1, nk - 1));   // stage 0 landed
+  Frag f0, f1;
+#pragma unroll
+  for (int i = 0; i < T4; ++i) { f0.a[i] = read_a(0, 0, i); f0.b[i] = read_b(0, 0, i); }
+  using yes = std::integral_constant<bool, true>;
+  using no = std::integral_constant<bool, false>;
+  // slice 0 of step ks reads slice 1 of the same slot; then stage ks+1 has landed (the stages issued after it
+  // may still be in flight) and every wave is done with slot ks (its fragments of both slices are in
+  // registers), so slice 1 reads slice 0 of step ks+1 and refills slot ks with step ks+STAGES
+  // registers), so slice 1 reads slice 0 of step ks+1 and starts refilling slot ks with step ks+STAGES; slice
+  // 0 of step ks+1 finishes that refill (the slot has been free since this barrier). Every transfer of stage
+  // s is issued before any of stage s+1, so a vmcnt bound of (STAGES-2) stages still means "stage ks+1 landed".
+  using none = std::integral_constant<int, 0>;
+  using half0 = std::integral_constant<int, 1>;
+  using half1 = std::integral_constant<int, 2>;
+  // (straight-line loop segments, not branches inside one loop: those made the register allocator move the
+  // accumulators through scratch)
+  int ks = 0;
+  if (STAGES < nk) {
+    slice(f0, f1, yes{}, none{}, 0, 1, 0);
+    dma_stage_sync<DPW, STAGES - 2>(STAGES - 2);
+    slice(f1, f0, yes{}, half0{}, 1, 0, STAGES);
+    for (ks = 1; ks + STAGES < nk; ++ks) {
+      slice(f0, f1, yes{}, half1{}, ks, 1, ks - 1 + STAGES);
+      dma_stage_sync<DPW, STAGES - 2>(STAGES - 2);
+      slice(f1, f0, yes{}, half0{}, ks + 1, 0, ks + STAGES);
+    }
+    // ks = nk - STAGES: the second half of the last stage
+    slice(f0, f1, yes{}, half1{}, ks, 1, ks - 1 + STAGES);
+    dma_stage_sync<DPW, STAGES - 2>(min(STAGES - 2, nk - 2 - ks));
+    slice(f1, f0, yes{}, none{}, ks + 1, 0, 0);
+    ++ks;
+  }
+  for (; ks + 1 < nk; ++ks) {
+    slice(f0, f1, yes{}, none{}, ks, 1, 0);
+    dma_stage_sync<DPW, STAGES - 2>(min(STAGES - 2, nk - 2 - ks));
+    slice(f1, f0, yes{}, none{}, ks + 1, 0, 0);
+  }
+  slice(f0, f1, yes{}, none{}, nk - 1, 1, 0);   // the last step
+  slice(f1, f0, no{}, none{}, 0, 0, 0);
+
+  __syncthreads();                              // every wave has read its last fragments from the ring
+  epi_trans<T4, T4, WT>(acc, &lds[0][0] + wave * 32 * (WT * 4 + 16), m0 + wm * WT, n0 + wn * WT, M, N, epi);
 }
 
 // ============================================================================ top-M per row
@@ -735,8 +898,8 @@ static sr_status launch_vocab_t(const sr_heads_desc& d, const void* z, const voi
     } else {
       constexpr int BM = 256;
       const int tm = (M + BM - 1) / BM;
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 2, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
-                dim3(512), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_q<SR_GQ_STAGES, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm), dim3(256), 0,
+                s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
     }
   } else {
     constexpr int BM = 128, BN = 128, BK = 32;
