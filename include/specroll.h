@@ -157,10 +157,10 @@ sr_status sr_tree_build(const sr_heads_desc* desc, const float* logits,
  * which equals ordinary causal attention at u's position of the sequence
  * prefix ++ path(u). Scores and softmax are fp32. For bf16 inputs the
  * probability-weighted sum over V runs on fp16 matrix cores with V converted
- * bf16 -> fp16: exact for |v| in [2^-14, 65280], within 2^-25 absolute below.
+ * bf16 -> fp16: exact for |v| in [2^-14, 65280], within 2^-24 absolute below.
  * A work item (trajectory, KV head, prefix chunk) whose largest |v| exceeds
  * 65280 (or is not finite) or lies below 2^-6 is recomputed with V in fp32,
- * so no finite bf16 V overflows and the conversion error stays below 2^-19 of
+ * so no finite bf16 V overflows and the conversion error stays below 2^-18 of
  * the item's V scale.
  */
 typedef struct {

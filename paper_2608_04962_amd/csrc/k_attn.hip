@@ -532,7 +532,7 @@ struct DmaGeom {
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
   static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
-  static constexpr int CPL = (CITEMS + 7 * 64 - 1) / (7 * 64);   // chunks per lane with >= 7 converting waves
+  static constexpr int CPL = CITEMS / 64;                // V chunks per lane of the converting (DMA) wave
   static_assert(CITEMS % 64 == 0, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
@@ -618,13 +618,14 @@ __device__ __forceinline__ void attn_item_dma(
   for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
   float m_run = -INFINITY, l_run = 0.f;
   // Roles. A row group holds at most ATT_ROWS - 32 rows (attn_plan), so wave n_act has no query rows: it
-  // issues all of the DMA, pacing itself on the memory system, and the other seven waves convert V (a
-  // single converting wave would hold the block at the barrier).
+  // issues all of the DMA, pacing itself on the memory system, and converts every V tile to fp16. It runs
+  // its own loop (the same barriers), so its conversion registers never share the compute waves' code.
+  // Measured per 64-key tile at the 7B shape: with the seven compute waves converting V, the second wave of
+  // each SIMD took 1.45k cycles for conversion and max, 2.3k for exponentials and next scores, 0.66k for
+  // P V, while the DMA wave waited 2.9k of its 4.6k at the barrier.
   const int n_act = min(ATT_NW - 1, (rend - rg * group_rows + 31) / 32);
   const bool wave_active = wave < n_act && !bad;
   const bool dma_wave = wave == n_act;
-  constexpr int n_tr = ATT_NW - 1;
-  const int tr_rank = wave < n_act ? wave : (wave == n_act ? -1 : wave - 1);
 
   const int n_pre = (key1 - key0 + ATT_KT - 1) / ATT_KT;
   const int n_tiles = bad ? 0 : n_pre + (last ? (T_ + ATT_KT - 1) / ATT_KT : 0);
@@ -704,39 +705,37 @@ __device__ __forceinline__ void attn_item_dma(
   // V of a tile, bf16 -> fp16 in place: every converting lane takes whole 16-byte chunks (their positions
   // do not matter). The reads (conv_load) are issued early and the converted chunks written later
   // (conv_store), so the LDS latency overlaps other work. The conversion is exact for magnitudes in
-  // [2^-14, 65280] and rounds smaller ones to fp16's subnormal step, an absolute error of at most 2^-25;
+  // [2^-14, 65280] and truncates smaller ones to fp16's subnormal step, an absolute error below 2^-24;
   // larger ones would overflow. Each converting lane keeps the largest magnitude pattern of everything it
   // converts (two 16-bit lanes per register): an item is recomputed with fp32 V when that exceeds 65280
   // (pattern 0x477f; inf and NaN included) or when the item's largest |v| is below 2^-6 (pattern 0x3c80),
-  // where 2^-25 would no longer be negligible against the scale of V.
+  // where 2^-24 would no longer be negligible against the scale of V.
   u32x4 cw[G::CPL];
   u16x2 vmag_hi = {0, 0};
   auto conv_load = [&](const unsigned char* v) __attribute__((always_inline)) {
-    if (tr_rank < 0) return;                    // the DMA wave
     int ln = lane;
     asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
 #pragma unroll
-    for (int k = 0; k < G::CPL; ++k) {
-      const int it = tr_rank * 64 + ln + k * n_tr * 64;
-      if (it < G::CITEMS) cw[k] = *(const u32x4*)(v + it * 16);
-    }
+    for (int k = 0; k < G::CPL; ++k) cw[k] = *(const u32x4*)(v + (ln + k * 64) * 16);
   };
   auto conv_store = [&](unsigned char* v) __attribute__((always_inline)) {
-    if (tr_rank < 0) return;
     int ln = lane;
     asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int k = 0; k < G::CPL; ++k) {
-      const int it = tr_rank * 64 + ln + k * n_tr * 64;
-      if (it < G::CITEMS) {
-        f16x8 h;
+      const int it = ln + k * 64;
+      {
+        // two values per instruction, rounding toward zero: exact for every value in fp16's normal range,
+        // within one subnormal step (2^-24) below it; out-of-range items are recomputed anyway
+        u32x4 h;
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          h[e] = (_Float16)bf2f((e & 1) ? (cw[k][e >> 1] >> 16) : (cw[k][e >> 1] & 0xffffu));
-        *(f16x8*)(v + it * 16) = h;
-#pragma unroll
-        for (int w = 0; w < 4; ++w)
-          vmag_hi = __builtin_elementwise_max(vmag_hi, __builtin_bit_cast(u16x2, cw[k][w] & 0x7fff7fffu));
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t x = cw[k][w];
+          h[w] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(__uint_as_float(x << 16),
+                                                                         __uint_as_float(x & 0xffff0000u)));
+          vmag_hi = __builtin_elementwise_max(vmag_hi, __builtin_bit_cast(u16x2, x & 0x7fff7fffu));
+        }
+        *(u32x4*)(v + it * 16) = h;
       }
     }
   };
@@ -873,17 +872,15 @@ __device__ __forceinline__ void attn_item_dma(
     }
   };
 
-  // ---- pipeline. step(i): wait for tile i+1, refill the slot of tile i-1 with tile i+3, convert V of
-  // tile i+1, then finish tile i while computing the scores of tile i+1 (slot of tile i: si).
+  // ---- pipeline. Compute waves, step(i): wait for tile i+1, then finish tile i while computing the scores of
+  // tile i+1 (slot of tile i: si). DMA wave, the same barriers: wait for tile i+1 (tiles i+2, i+3 may stay in
+  // flight), read tile i+1's V, refill the slot of tile i-1 with tile i+3 (whose issue stalls overlap the
+  // reads), convert tile i+1's V; it is consumed after the next barrier.
   f32x16 sa[2], sb[2];
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
-    const int sn_ = (si + 1) & 3, sf = (si + 3) & 3;
-    attn_sync<D>(dma_wave, i + 2 < n_tiles);
-    if (dma_wave && i + 3 < n_tiles) issue(i + 3, ring[sf]);
-    const bool cv = i + 1 < n_tiles;
-    if (cv) conv_load(ring[sn_] + G::TILE);
+    const int sn_ = (si + 1) & 3;
+    attn_sync<D>(false, false);
     if (wave_active) finish_max(i, s);
-    if (cv) conv_store(ring[sn_] + G::TILE);
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
     if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn);
   };
@@ -891,19 +888,31 @@ __device__ __forceinline__ void attn_item_dma(
     if (dma_wave) {
       issue(0, ring[0]);
       if (n_tiles > 1) issue(1, ring[1]);
-    }
-    attn_sync<D>(dma_wave, n_tiles > 1);     // tile 0 landed (tile 1 may be in flight)
-    if (dma_wave && n_tiles > 2) issue(2, ring[2]);
-    conv_load(ring[0] + G::TILE);
-    conv_store(ring[0] + G::TILE);
-    if (wave_active) qk(ring[0], sa);
-    int si = 0;
-    for (int i = 0; i < n_tiles; i += 2) {
-      step(i, si, sa, sb);
-      si = (si + 1) & 3;
-      if (i + 1 < n_tiles) {
-        step(i + 1, si, sb, sa);
+      attn_sync<D>(true, n_tiles > 1);          // tile 0 landed (tile 1 may be in flight)
+      if (n_tiles > 2) issue(2, ring[2]);
+      conv_load(ring[0] + G::TILE);
+      conv_store(ring[0] + G::TILE);
+      int si = 0;
+      for (int i = 0; i < n_tiles; ++i) {
+        const int sn_ = (si + 1) & 3, sf = (si + 3) & 3;
+        attn_sync<D>(true, i + 2 < n_tiles);
+        const bool cv = i + 1 < n_tiles;
+        if (cv) conv_load(ring[sn_] + G::TILE);
+        if (i + 3 < n_tiles) issue(i + 3, ring[sf]);
+        if (cv) conv_store(ring[sn_] + G::TILE);
         si = (si + 1) & 3;
+      }
+    } else {
+      attn_sync<D>(false, false);               // tile 0 landed and converted
+      if (wave_active) qk(ring[0], sa);
+      int si = 0;
+      for (int i = 0; i < n_tiles; i += 2) {
+        step(i, si, sa, sb);
+        si = (si + 1) & 3;
+        if (i + 1 < n_tiles) {
+          step(i + 1, si, sb, sa);
+          si = (si + 1) & 3;
+        }
       }
     }
   }
@@ -914,7 +923,7 @@ __device__ __forceinline__ void attn_item_dma(
   {
     uint32_t hi = max((uint32_t)vmag_hi[0], (uint32_t)vmag_hi[1]);
     hi = (uint32_t)warp_max_i((int)hi);
-    if (tr_rank >= 0 && lane == 0) atomicMax(&meta.vwide, (int)hi);
+    if (dma_wave && lane == 0) atomicMax(&meta.vwide, (int)hi);
     __syncthreads();
     if (threadIdx.x == 0 && n_tiles > 0 && (meta.vwide > 0x477f || meta.vwide < 0x3c80)) {
       const unsigned k = atomicAdd(redo, 1u);
