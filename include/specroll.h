@@ -191,9 +191,10 @@ size_t sr_tree_verify_attn_workspace(const sr_attn_desc* desc);
  * block_table entries past its last page. Invalid trajectory (ctx_len out of
  * range, a page id outside [0,num_blocks), bad topology): out and lse are NaN.
  * Workspace: the partial results of trajectories split into prefix chunks and,
- * for bf16, the work-item counter of the persistent kernel and the list of work
- * items to recompute with fp32 V, whose counters the call zeroes itself with a
- * kernel on the stream (no initialisation by the caller, no memset). Two calls
+ * for bf16, the work-item counter of the persistent kernel, the list of work
+ * items to recompute with fp32 V and the work items ordered by length (longest
+ * first), all of which the call rebuilds itself with a kernel on the stream
+ * (no initialisation by the caller, no memset). Two calls
  * that share a workspace must not run concurrently (on one stream they don't).
  */
 sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
@@ -207,8 +208,8 @@ sr_status sr_tree_verify_attn(const sr_attn_desc* desc,
  * sr_tree_verify_attn without a workspace, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc). Arguments and results as sr_tree_verify_attn. The
- * scratch the call needs (the chunk partials, the work-item counter and the
- * fp32-V recomputation list: sr_tree_verify_attn_workspace bytes) lives in a
+ * scratch the call needs (the chunk partials, the work-item counter and list,
+ * the fp32-V recomputation list: sr_tree_verify_attn_workspace bytes) lives in a
  * static device array of SR_ATTN_NOALLOC_MAX_BYTES per GPU, which the library
  * holds on every GPU it runs on until the process ends; the call itself
  * allocates nothing. A request that needs more returns SR_ERR_UNSUPPORTED with

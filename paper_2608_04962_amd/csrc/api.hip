@@ -178,7 +178,7 @@ const char* sr_last_error(void) { return g_err.c_str(); }
 const char* sr_version(void) { return "specroll-mi355x 0.1 (gfx950)"; }
 
 const char* sr_kernel_names(void) {
-  return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_attn_reset;"
+  return "sr_clip_ln;sr_head_gemm;sr_vocab_gemm;sr_group_max;sr_topm;sr_topm_full;sr_tree_build;sr_attn_order;"
          "sr_tree_attn;sr_attn_redo;sr_attn_combine;sr_tree_accept;sr_commit_path;sr_reflex_feedback;"
          "sr_reflex_correct";
 }

@@ -57,6 +57,10 @@ __device__ __forceinline__ void lds_dma16_sv(uint32_t voff, const void* sbase, u
                : "memory", "m0");
 }
 
+// workgroup barrier ordering LDS only: this wave's LDS operations complete, global memory operations may
+// still be in flight (unlike __syncthreads, which also waits for them)
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // wait until at most N of this wave's vector memory operations (LDS DMA included) are outstanding
 template <int N> __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt");

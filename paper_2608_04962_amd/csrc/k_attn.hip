@@ -39,7 +39,7 @@ constexpr int ATT_KT = 64;             // keys per LDS tile
 constexpr int ATT_NW = 8;              // waves per block
 constexpr int ATT_RB = 1;              // 32-row query blocks per wave
 constexpr int ATT_ROWS = ATT_NW * ATT_RB * 32;  // query rows per block
-constexpr int ATT_CHUNK_PAGES = 192;   // most prefix pages per work item (3072 tokens): with many
+constexpr int ATT_CHUNK_PAGES = 256;   // most prefix pages per work item (4096 tokens): with many
                                        // (trajectory, KV head) pairs; 128 or 32 with fewer (attn_plan)
 constexpr int ATT_BS = 16;             // tokens per page
 
@@ -969,10 +969,11 @@ __device__ __forceinline__ void attn_item_dma(
   }
 }
 
-// Persistent blocks (one per CU) take work items from a counter in item order: every first chunk, then
-// every second chunk, and so on, so the long items start first and the short last chunks fill the tail;
-// items past a trajectory's chunk count return at once. Every wave runs the same iterations (the item
-// is broadcast through LDS), and the loop ends for all once the counter passes n_items.
+// Persistent blocks (one per CU) take work items from a counter, in the order k_attn_order lists them
+// (most tiles first, so the last items to start are the shortest and the blocks end close together). Every
+// wave runs the same iterations (the item is broadcast through LDS), and the loop ends for all once the
+// counter passes the list. Between items the block meets with LDS-only barriers: the previous item's
+// global stores need not have landed before the next item starts.
 template <int D>
 __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache, const bf16_t* __restrict__ v_cache,
@@ -981,24 +982,76 @@ __global__ __launch_bounds__(ATT_NW * 64) void k_tree_attn_dma(
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_ml, int B_, int T_, int Hq,
     int Hkv, int max_blocks, int num_blocks, float scale_log2, int R, int Rpad, int row_groups, int group_rows,
     int n_chunks_max, int cp, int n_items, unsigned* __restrict__ work) {
-  // work[0]: item counter; work[1], work[2..]: count and items of the fp32-V redo list
+  // work: item counter, then the redo list (count, items), the number of listed items and the list
   __shared__ __attribute__((aligned(1024))) unsigned char ring[4][2 * DmaGeom<D>::TILE];
   __shared__ AttnMeta meta;
   __shared__ int s_item;
+  const unsigned n_live = work[2 + n_items];
+  const unsigned* order = work + 3 + n_items;
   for (;;) {
-    __syncthreads();                     // every wave is done with the previous item (ring, meta, s_item)
-    if (threadIdx.x == 0) s_item = (int)atomicAdd(work, 1u);
-    __syncthreads();
+    lds_barrier();                       // every wave is done with the previous item (ring, meta, s_item)
+    if (threadIdx.x == 0) {
+      const unsigned k = atomicAdd(work, 1u);
+      s_item = k < n_live ? (int)order[k] : -1;
+    }
+    lds_barrier();
     const int item = __builtin_amdgcn_readfirstlane(s_item);   // uniform: its derived values stay scalar
-    if (item >= n_items) break;
+    if (item < 0) break;
     attn_item_dma<D>(item, ring, meta, q, k_cache, v_cache, block_table, ctx_len, k_tree, v_tree, parents, out,
                      lse, part_o, part_ml, B_, T_, Hq, Hkv, max_blocks, num_blocks, scale_log2, R, Rpad,
                      row_groups, group_rows, n_chunks_max, cp, work + 1);
   }
 }
 
-__global__ void k_attn_work_reset(unsigned* __restrict__ work) {
-  if (threadIdx.x < 2) work[threadIdx.x] = 0u;   // item counter, redo count
+// The work list of the persistent kernel: one block computes every item's tile count from ctx_len and
+// counting-sorts the items by it, most tiles first (greedy list scheduling then ends the blocks close
+// together). Items past a trajectory's chunk count are left out; a trajectory with an invalid ctx_len keeps
+// its first item, which writes its NaN rows. Items of equal count keep no particular order (no result
+// depends on it). Also zeroes the item counter and the redo count. work: [0] item counter, [1] redo count,
+// [2, 2 + n_items) redo items, [2 + n_items] listed items, [3 + n_items, ...) the list.
+constexpr int ATT_ORDER_BUCKETS = 64;
+__global__ __launch_bounds__(1024) void k_attn_order(const int32_t* __restrict__ ctx_len, unsigned* __restrict__ work,
+                                                     int B_, int T_, int Hkv, int row_groups, int max_blocks, int cp,
+                                                     int n_items) {
+  __shared__ unsigned cnt[ATT_ORDER_BUCKETS];
+  const int tid = threadIdx.x;
+  if (tid < ATT_ORDER_BUCKETS) cnt[tid] = 0u;
+  if (tid < 2) work[tid] = 0u;
+  __syncthreads();
+  // bucket of an item: ATT_ORDER_BUCKETS - 1 - min(tiles, ATT_ORDER_BUCKETS - 1), or -1 when it has no work
+  auto bucket = [&](int item) -> int {
+    const int bg = item / row_groups;
+    const int b = (bg / Hkv) % B_, c = bg / (Hkv * B_);
+    const int Lraw = ctx_len[b];
+    if (Lraw < 0 || Lraw > max_blocks * ATT_BS) return c == 0 ? ATT_ORDER_BUCKETS - 1 : -1;
+    const int pages = (Lraw + ATT_BS - 1) / ATT_BS;
+    const int n_chunks = max(1, (pages + cp - 1) / cp);
+    if (c >= n_chunks) return -1;
+    const int page0 = c * cp, page1 = min(pages, page0 + cp);
+    const int keys = min(Lraw, page1 * ATT_BS) - page0 * ATT_BS;
+    const int tiles = (keys + ATT_KT - 1) / ATT_KT + (c == n_chunks - 1 ? (T_ + ATT_KT - 1) / ATT_KT : 0);
+    return ATT_ORDER_BUCKETS - 1 - min(tiles, ATT_ORDER_BUCKETS - 1);
+  };
+  for (int k = tid; k < n_items; k += blockDim.x) {
+    const int bk = bucket(k);
+    if (bk >= 0) atomicAdd(&cnt[bk], 1u);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    unsigned run = 0;
+    for (int i = 0; i < ATT_ORDER_BUCKETS; ++i) {
+      const unsigned c = cnt[i];
+      cnt[i] = run;
+      run += c;
+    }
+    work[2 + n_items] = run;
+  }
+  __syncthreads();
+  unsigned* order = work + 3 + n_items;
+  for (int k = tid; k < n_items; k += blockDim.x) {
+    const int bk = bucket(k);
+    if (bk >= 0) order[atomicAdd(&cnt[bk], 1u)] = (unsigned)k;
+  }
 }
 
 // Merge the chunk partials of every (trajectory, KV head) that was split.
@@ -1089,9 +1142,10 @@ AttnPlan attn_plan(const sr_attn_desc& d) {
   const size_t rows = (size_t)d.B * d.Hkv * p.n_chunks * p.Rpad;
   p.part_o_bytes = p.n_chunks > 1 ? rows * d.D * sizeof(float) : 0;
   p.part_ml_bytes = p.n_chunks > 1 ? rows * 2 * sizeof(float) : 0;
-  // bf16: the persistent kernel's item counter, then the count and items of the fp32-V redo list
+  // bf16: the persistent kernel's item counter, the count and items of the fp32-V redo list, the number of
+  // listed items and the list (k_attn_order)
   p.n_items = (long long)d.B * d.Hkv * p.row_groups * p.n_chunks;
-  p.work_bytes = d.dtype == SR_BF16 ? (size_t)(2 + p.n_items) * sizeof(unsigned) : 0;
+  p.work_bytes = d.dtype == SR_BF16 ? (size_t)(3 + 2 * p.n_items) * sizeof(unsigned) : 0;
   return p;
 }
 
@@ -1122,7 +1176,8 @@ static sr_status launch_attn_t(const sr_attn_desc& d, const AttnPlan& p, const v
   if constexpr (sizeof(T) == 2) {
     const long long n_items = (long long)grid.x * grid.y;
     if (n_items > INT32_MAX / 2) return SR_ERR_INVALID;
-    SR_LAUNCH("sr_attn_reset", k_attn_work_reset, dim3(1), dim3(64), 0, s, work);
+    SR_LAUNCH("sr_attn_order", k_attn_order, dim3(1), dim3(1024), 0, s, cl, work, d.B, d.T, d.Hkv, p.row_groups,
+              d.max_blocks, p.chunk_pages, (int)n_items);
     const int nb = (int)std::min<long long>(n_items, cu_count());
     SR_LAUNCH("sr_tree_attn", (k_tree_attn_dma<D>), dim3(nb), dim3(ATT_NW * 64), 0, s, (const T*)q, (const T*)kc,
               (const T*)vc, bt, cl, (const T*)kt, (const T*)vt, par, out, lse, po, pml, d.B, d.T, d.Hq, d.Hkv,

@@ -51,16 +51,17 @@ def test_config0_all_nodes():
 
 @pytest.mark.parametrize("seed", [0, 1])
 def test_bf16_multi_chunk_ragged(seed):
-    # contexts straddle the 2048-token chunk size so the split/combine path and ragged tails run
+    # 10 (trajectory, KV head) pairs take 32-page (512-token) chunks: contexts up to 5000 tokens run the
+    # split/combine path over up to ten chunks with ragged tails
     cfg = synth.scaled(synth.SHAPE_7B, B=5, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 1, 5000))
     inp = synth.attn_inputs(cfg, seed=seed)
     _check(inp)
 
 
 def test_bf16_long_chunks_all_nodes():
-    # 512 (trajectory, KV head) pairs select 192-page prefix chunks: contexts of 2900-6200 tokens take one
+    # 512 (trajectory, KV head) pairs select 256-page prefix chunks: contexts of 2900-9000 tokens take one
     # to three chunks, with ragged tails; every node of every trajectory is compared
-    cfg = synth.scaled(synth.SHAPE_7B, B=128, T=2, depth=1, ctx=("uniform", 2900, 6200))
+    cfg = synth.scaled(synth.SHAPE_7B, B=128, T=2, depth=1, ctx=("uniform", 2900, 9000))
     _check(synth.attn_inputs(cfg, seed=5))
 
 
@@ -100,6 +101,12 @@ def test_invalid_inputs_give_nan_rows_only_for_that_trajectory():
     inp2["parents"][0, 3] = 5                             # not an earlier node
     out2, _ = _run_gpu(inp2)
     assert np.isnan(out2[0]).all() and np.isfinite(out2[1:]).all()
+    inp3 = synth.attn_inputs(cfg, seed=9)
+    inp3["ctx_len"] = inp3["ctx_len"].copy()
+    inp3["ctx_len"][1] = -1                               # negative length
+    out3, lse3 = _run_gpu(inp3)
+    assert np.isnan(out3[1]).all() and np.isnan(lse3[1]).all()
+    assert np.isfinite(out3[0]).all() and np.isfinite(out3[2]).all()
 
 
 def test_deterministic():
