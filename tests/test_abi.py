@@ -106,7 +106,7 @@ def test_workspace_queries_are_consistent():
     d2 = _lib.AttnDesc(2, 8, 4, 2, 64, 16, 10, 20, _lib.SR_BF16, 0.125)   # 2 x 2 (trajectory, KV head) items
     assert _lib.lib().sr_tree_verify_attn_workspace(C.byref(d2)) == 256
     d3 = _lib.AttnDesc(128, 32, 28, 4, 128, 16, 512, 40000, _lib.SR_F32, 0.088)
-    n_items = 128 * 4 * 3                                               # 224 rows: one group; 192-page chunks
+    n_items = 128 * 4 * 2                                               # 224 rows: one group; 256-page chunks
     assert _lib.lib().sr_tree_verify_attn_workspace(C.byref(d)) == \
         _lib.lib().sr_tree_verify_attn_workspace(C.byref(d3)) + (3 + 2 * n_items) * 4 // 256 * 256 + 256
     assert _lib.lib().sr_tree_accept_workspace(C.byref(_lib.AcceptDesc(2, 8, 512, 3, 0, 1.0, 1.0))) == 0
