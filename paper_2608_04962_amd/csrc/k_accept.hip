@@ -33,6 +33,7 @@ constexpr int ACC_NW = 16;
 constexpr int ACC_NT = ACC_NW * 64;
 constexpr int ACC_CH = 512;                  // tokens per chunk = 64 lanes x 8
 constexpr int ACC_MAX_CHUNKS = 512;          // V <= 262144
+static_assert(SR_MAX_TREE <= ACC_NT, "one tree node per thread at set-up");
 // Row access. A lane's 8 consecutive tokens load as one Raw value (kept packed while in flight: bf16
 // rows take half the registers, so a wave keeps GROUP = 8 chunks' loads in flight instead of 4) and
 // unpack to fp32 when used; ninf() unpacks to eight -inf (lanes past the row).
@@ -80,6 +81,8 @@ struct AccSmem {
   double cscale[ACC_MAX_CHUNKS];
   int kids[SR_MAX_TREE];
   double kpt[SR_MAX_TREE];   // unnormalised target weight of each child's token at the current node
+  float kx[SR_MAX_TREE];     // plain walk: each child's logit, taken from the row pass
+  int ktok[SR_MAX_TREE];     // the current node's children's tokens (kids order)
   double xsum[ACC_MAX_CHUNKS];         // chunks holding a child: the weight of their other tokens
   unsigned char xflag[ACC_MAX_CHUNKS]; // the chunk holds a child of the current node
   double S;
@@ -116,8 +119,12 @@ __device__ __forceinline__ float tilt(float x, float invtau, float m) {
   return __builtin_amdgcn_exp2f(__builtin_fmaf(x, __fmul_rn(invtau, kLog2e), -__fmul_rn(m, kLog2e)));
 }
 
+// Row pass of the plain walk. With m > 0 (the node's children in sm.kids, their chunks flagged in xflag)
+// the same pass also sums each flagged chunk over its tokens other than the children -- exactly what
+// outside_mass would sum, from the same loaded values -- and keeps the children's logits in sm.kx; the
+// final combine then sets xsum (scaled) and S_out as outside_mass does.
 template <typename T>
-__device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
+__device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float invtau, int m_kids) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
   constexpr int GRP = RowLoad<T>::GROUP;
@@ -127,6 +134,13 @@ __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float i
     for (int gi = 0; gi < GRP; ++gi) {
       const int base = (c0 + gi) * ACC_CH + lane * 8;
       w[gi] = (c0 + gi < nch && base < V) ? RowLoad<T>::raw(row + base) : RowLoad<T>::ninf();
+    }
+    // the group's chunk flags in one LDS read (byte gi: chunk c0 + gi holds a child; entries past nch are
+    // never tested)
+    unsigned long long gflags = 0;
+    if (m_kids > 0) {
+      if constexpr (GRP == 8) gflags = *(const unsigned long long*)&sm.xflag[c0];
+      else gflags = *(const uint32_t*)&sm.xflag[c0];
     }
     // One reference max for the GRP chunks of this group: their max of x * invtau (rounding is monotone,
     // so the max of the raw logits times invtau > 0 is the max of the products). Every consumer weighs a
@@ -158,20 +172,53 @@ __device__ void row_stats(AccSmem& sm, const T* __restrict__ row, int V, float i
     int j;
     const float s = wave_sum_scatter<GRP>(a, j);
     if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) { sm.cmax[c0 + j] = m; sm.csum[c0 + j] = (double)s; }
+    if (m_kids > 0 && gflags != 0) {
+#pragma unroll
+      for (int gi = 0; gi < GRP; ++gi) {
+        const int c = c0 + gi;
+        if (c >= nch || ((gflags >> (8 * gi)) & 0xffu) == 0) continue;   // uniform per wave
+        const int base = c * ACC_CH + lane * 8;
+        float x[8];
+        RowLoad<T>::unpack(w[gi], x);
+        unsigned excl = 0;                        // this lane's tokens that are children
+        for (int k = 0; k < m_kids; ++k) {
+          const int v = sm.ktok[k];
+          if (v >= base && v < base + 8) {
+            excl |= 1u << (v - base);
+            sm.kx[k] = x[v - base];
+          }
+        }
+        double xs = 0.0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (!((excl >> e) & 1u) && x[e] != -INFINITY) xs += (double)tilt(x[e], invtau, m);
+        xs = wave_sum_f64(xs);
+        if (lane == 0) sm.xsum[c] = xs;           // scaled by cscale[c] below
+      }
+    }
   }
   __syncthreads();
   if (wave == 0) {
     float ml = -INFINITY;
     for (int c = lane; c < nch; c += 64) ml = fmaxf(ml, sm.cmax[c]);
     const float M = wave_max_f32(ml);
-    double sl = 0.0;
+    double sl = 0.0, so = 0.0;
     for (int c = lane; c < nch; c += 64) {
       const double sc = exp((double)sm.cmax[c] - (double)M);
       sm.cscale[c] = sc;
-      sl += sm.csum[c] * sc;
+      const double a = sm.csum[c] * sc;
+      sl += a;
+      if (m_kids > 0 && sm.xflag[c]) {
+        const double xs = sm.xsum[c] * sc;
+        sm.xsum[c] = xs;
+        so += xs;
+      } else {
+        so += a;
+      }
     }
     const double S = wave_sum_f64(sl);
-    if (lane == 0) { sm.S = S; sm.M = M; sm.nk_on = 0; }
+    const double So = wave_sum_f64(so);
+    if (lane == 0) { sm.S = S; sm.S_out = So; sm.M = M; sm.nk_on = 0; }
   }
   __syncthreads();
 }
@@ -712,13 +759,22 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   int32_t* an = acc_nodes + (size_t)b * max_depth;
   int32_t* ot = out_tokens + (size_t)b * (max_depth + 1);
 
+  // the node inputs are loaded before the topology is checked, so their latency overlaps it (T <= the
+  // block size: one node per thread)
+  int v_in = 0;
+  float cl_in = 0.f, ua_in = 0.f;
+  if (tid < T_) {
+    v_in = tokens[(size_t)b * T_ + tid];
+    cl_in = child_logit[(size_t)b * T_ + tid];
+    ua_in = u_acc[(size_t)b * T_ + tid];
+  }
   bool ok = tree_setup<SR_MAX_TREE>(sm.tree, parents + (size_t)b * T_, T_);
   if (ok) {
-    for (int c = tid; c < T_; c += ACC_NT) {
-      const int v = tokens[(size_t)b * T_ + c];
+    if (tid < T_) {
+      const int c = tid, v = v_in;
       sm.tok[c] = v;
-      sm.cl[c] = child_logit[(size_t)b * T_ + c];
-      sm.ua[c] = u_acc[(size_t)b * T_ + c];
+      sm.cl[c] = cl_in;
+      sm.ua[c] = ua_in;
       if (c > 0 && (v < 0 || v >= V)) atomicOr(&sm.tree.bad, 1);
       if (sm.tree.depth[c] > max_depth) atomicOr(&sm.tree.bad, 1);
     }
@@ -746,25 +802,43 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   int n_acc = 0;
   int u = 0;
   const float Ufin = u_fin[b];
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
   while (true) {
     const T* row = base + (size_t)u * V;
+    // the node's children in node order (ballot compaction) and, for the plain walk, the chunks that
+    // hold them
+    if (wave == 0) {
+      if (!NUC) {                                // cleared before the children set theirs (one wave's LDS
+        for (int c = lane; c < nch; c += 64) sm.xflag[c] = 0;   // writes complete in order)
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+      int n = 0;
+      for (int c0 = 0; c0 < T_; c0 += 64) {
+        const int c = c0 + lane;
+        const bool kid = c > u && c < T_ && sm.tree.parent[c] == u;
+        const unsigned long long bal = __ballot(kid);
+        if (kid) {
+          const int slot = n + __popcll(bal & ((1ull << lane) - 1ull));
+          const int v = sm.tok[c];
+          sm.kids[slot] = c;
+          sm.ktok[slot] = v;
+          if (!NUC) sm.xflag[v / ACC_CH] = 1;
+        }
+        n += __popcll(bal);
+      }
+      if (lane == 0) sm.nkid = n;
+    }
+    __syncthreads();
+    const int m = sm.nkid;
     if constexpr (NUC) {
       row_stats_nuc<T>(sm, row, V, invtau);
       nucleus<T>(sm, row, V, invtau, top_p);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
       nuc_masked_sums<T>(sm, row, V, invtau);   // chunk sums over the nucleus; outside_mass sums them to S
+      outside_mass<T, NUC>(sm, row, V, invtau, m);
     } else {
-      row_stats<T>(sm, row, V, invtau);
+      row_stats<T>(sm, row, V, invtau, m);     // with the children's chunks and logits
     }
-    if (tid == 0) {
-      int n = 0;
-      for (int c = u + 1; c < T_; ++c)
-        if (sm.tree.parent[c] == u) sm.kids[n++] = c;
-      sm.nkid = n;
-    }
-    __syncthreads();
-    const int m = sm.nkid;
-    outside_mass<T, NUC>(sm, row, V, invtau, m);
     if (wave == 0) {
       // residual on the children (2 per lane) and the mass outside them, float64
       double r[2], lg[2];
@@ -774,7 +848,14 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
         r[s] = 0.0;
         lg[s] = -INFINITY;
         if (k < m) {
-          const double pt = ptilde(sm, row, sm.tok[sm.kids[k]], invtau);
+          double pt;
+          if constexpr (NUC) {
+            pt = ptilde(sm, row, sm.tok[sm.kids[k]], invtau);
+          } else {                              // ptilde of the logit the row pass kept
+            const float x = sm.kx[k];
+            const int c = sm.tok[sm.kids[k]] / ACC_CH;
+            pt = x == -INFINITY ? 0.0 : (double)tilt(x, invtau, sm.cmax[c]) * sm.cscale[c];
+          }
           sm.kpt[k] = pt;
           r[s] = pt / sm.S;
           lg[s] = (double)sm.cl[sm.kids[k]];
@@ -847,7 +928,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
       nuc_masked_sums<T>(sm, lrow, V, invtau);
     } else {
-      row_stats<T>(sm, lrow, V, invtau);
+      row_stats<T>(sm, lrow, V, invtau, 0);
     }
     if (wave == 0) draw<T>(sm, lrow, V, invtau, 0, Ufin);
     __syncthreads();
