@@ -40,6 +40,8 @@ def _check(inp, nodes=None):
     assert err.max() <= tol, f"max row error {err.max():.3e} > {tol}"
     # lse (natural log of the softmax normaliser): absolute error within the same bar
     lerr = np.abs(lse[sel] - rl[sel]).max()
+    print(f"[parity] attention {inp['cfg'].name}: {int(sel.sum() // inp['cfg'].Hq)} nodes, max row rel err "
+          f"{err.max():.2e}, max lse abs err {lerr:.2e} (bar {tol})", flush=True)
     assert lerr <= tol, f"lse error {lerr:.3e} > {tol}"
     assert np.isfinite(out).all()
     return err.max()

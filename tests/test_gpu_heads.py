@@ -91,6 +91,8 @@ def _full_size(cfg, rows, tree_rows):
     ref = _oracle_heads(inp, rows=rows)
     _check_z(inp, z[rows], ref)
     lerr = row_rel_err(lg[rows].reshape(-1, cfg.V), ref["logits"].reshape(-1, cfg.V))
+    print(f"[parity] heads {cfg.name}: {len(rows)} trajectories, max logits row rel err {lerr.max():.2e} (bar 2e-3)",
+          flush=True)
     assert lerr.max() <= 2e-3, lerr.max()
     _check_fused_tree(inp, tok, cl, lg, tree_rows)
     return inp
