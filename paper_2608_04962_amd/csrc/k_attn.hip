@@ -757,38 +757,34 @@ __device__ __forceinline__ void attn_item_dma(
   // mask, online softmax and O^T += V^T P^T for tile i (scores s); the next tile's scores (K in nks) are
   // computed into sn in the same basic block as this tile's exponentials
   float f_muse = 0.f, f_alpha = 1.f;
-  // mask and max of tile i's scores, the new reference max and the rescale of the accumulator
-  auto finish_max = [&](int i, f32x16 (&s)[2]) {
+  // mask of tile i's scores (a whole prefix tile needs none)
+  auto tile_full = [&](int i) -> bool { return i < n_pre && key0 + i * ATT_KT + ATT_KT <= key1; };
+  auto mask_tile = [&](int i, f32x16 (&s)[2]) {
     const bool tree = i >= n_pre;
     const int t0 = tree ? (i - n_pre) * ATT_KT : key0 + i * ATT_KT;
-    const bool full = !tree && t0 + ATT_KT <= key1;
-    if (!full) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const int kb = t0 + kt * 32;
-        uint32_t v;
-        if (tree) {
-          v = (row_ok && last) ? meta.anc[my_t][kb >> 5] : 0u;
-        } else {
-          const int nv = key1 - kb;
-          v = nv >= 32 ? 0xffffffffu : (nv <= 0 ? 0u : ((1u << nv) - 1u));
-        }
-        v >>= 4 * half;
+    for (int kt = 0; kt < 2; ++kt) {
+      const int kb = t0 + kt * 32;
+      uint32_t v;
+      if (tree) {
+        v = (row_ok && last) ? meta.anc[my_t][kb >> 5] : 0u;
+      } else {
+        const int nv = key1 - kb;
+        v = nv >= 32 ? 0xffffffffu : (nv <= 0 ? 0u : ((1u << nv) - 1u));
+      }
+      v >>= 4 * half;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool ok = (v >> (8 * (r >> 2) + (r & 3))) & 1u;
-          s[kt][r] = ok ? s[kt][r] : -INFINITY;
-        }
+      for (int r = 0; r < 16; ++r) {
+        const bool ok = (v >> (8 * (r >> 2) + (r & 3))) & 1u;
+        s[kt][r] = ok ? s[kt][r] : -INFINITY;
       }
     }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+  };
+  // from a lane's max of a tile's (masked) scores: the row max, the new reference max and the accumulator
+  // rescale. The reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
+  // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled.
+  auto commit_max = [&](float mx) {
     mx = max_halves(mx);
-    // the reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
-    // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled
     const float tmax = mx * scale_log2;
     const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
@@ -801,9 +797,21 @@ __device__ __forceinline__ void attn_item_dma(
     f_muse = m_use;
     f_alpha = alpha;
   };
+  auto finish_max = [&](int i, f32x16 (&s)[2]) {
+    if (!tile_full(i)) mask_tile(i, s);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+    commit_max(mx);
+  };
   // exponentials of tile i (scores s), computed in one basic block with the scores of the next tile (K in
-  // nks, into sn), then O^T += V^T P^T with V of tile i (vs)
-  auto finish_rest = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2]) {
+  // nks, into sn), then O^T += V^T P^T with V of tile i (vs); with `next`, the mask and max of the next
+  // tile's scores follow, the max spread over the P V MFMAs (the matrix core works while the vector ALU
+  // reduces), and the rescale after them
+  auto finish_rest = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2],
+                         bool next) {
     const float m_use = f_muse, alpha = f_alpha;
     // From here on one basic block, laid out by hand with scheduling fences: each step issues the
     // K fragment reads one step ahead, two score MFMAs of the next tile and 32/NQF of this tile's
@@ -861,6 +869,9 @@ __device__ __forceinline__ void attn_item_dma(
       }
       return (f16x8){part[0][0], part[0][1], part[0][2], part[0][3], part[1][0], part[1][1], part[1][2], part[1][3]};
     };
+    if (next && !tile_full(i + 1)) mask_tile(i + 1, sn);
+    constexpr int MPJ = 32 / NPV;               // next-tile scores maxed per P V MFMA
+    float mx = -INFINITY;
     vf[0] = vread(0);
     vf[1] = vread(1);
 #pragma unroll
@@ -868,8 +879,11 @@ __device__ __forceinline__ void attn_item_dma(
       if (j + 2 < NPV) vf[(j + 2) % 3] = vread(j + 2);
       const int kt = j / (2 * NDT), kq = (j / NDT) & 1, dt = j % NDT;
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[j % 3], pf[kt][kq], o[dt], 0, 0, 0);
+#pragma unroll
+      for (int e = j * MPJ; e < (j + 1) * MPJ; ++e) mx = fmaxf(mx, sn[e >> 4][e & 15]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (next) commit_max(mx);
   };
 
   // ---- pipeline. Compute waves, step(i): wait for tile i+1, then finish tile i while computing the scores of
@@ -880,9 +894,8 @@ __device__ __forceinline__ void attn_item_dma(
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
     const int sn_ = (si + 1) & 3;
     attn_sync<D>(false, false);
-    if (wave_active) finish_max(i, s);
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
-    if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn);
+    if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn, i + 1 < n_tiles);
   };
   if (n_tiles > 0) {
     if (dma_wave) {
@@ -904,7 +917,10 @@ __device__ __forceinline__ void attn_item_dma(
       }
     } else {
       attn_sync<D>(false, false);               // tile 0 landed and converted
-      if (wave_active) qk(ring[0], sa);
+      if (wave_active) {
+        qk(ring[0], sa);
+        finish_max(0, sa);
+      }
       int si = 0;
       for (int i = 0; i < n_tiles; i += 2) {
         step(i, si, sa, sb);
