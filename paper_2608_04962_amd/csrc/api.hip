@@ -40,7 +40,10 @@ struct Prof {
 };
 static Prof g_prof;
 
-LaunchGuard::LaunchGuard(const char* n, hipStream_t s) : name(n), stream(s), slot(-1) {
+// A timed launch gets a start and a stop event that the kernel's dispatch records itself
+// (hipExtLaunchKernelGGL): the timing adds no commands to the stream between kernels.
+LaunchGuard::LaunchGuard(const char* n, hipStream_t s)
+    : name(n), stream(s), slot(-1), ev_start(nullptr), ev_stop(nullptr) {
   if (g_prof.on && strstr(n, g_prof.pat.c_str()) != nullptr && g_prof.used < Prof::kMax) {
     if ((int)g_prof.start.size() <= g_prof.used) {
       hipEvent_t a, b;
@@ -49,16 +52,14 @@ LaunchGuard::LaunchGuard(const char* n, hipStream_t s) : name(n), stream(s), slo
       g_prof.stop.push_back(b);
     }
     slot = g_prof.used;
-    (void)hipEventRecord(g_prof.start[slot], s);
+    ev_start = g_prof.start[slot];
+    ev_stop = g_prof.stop[slot];
   }
 }
 
 sr_status LaunchGuard::done() {
   hipError_t e = hipGetLastError();
-  if (slot >= 0) {
-    (void)hipEventRecord(g_prof.stop[slot], stream);
-    ++g_prof.used;
-  }
+  if (slot >= 0) ++g_prof.used;
   if (e != hipSuccess) {
     set_error("launch of %s failed: %s", name, hipGetErrorString(e));
     return SR_ERR_HIP;

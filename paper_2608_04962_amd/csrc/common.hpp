@@ -1,6 +1,7 @@
 // Shared device/host helpers of the gfx950 speculative-verification kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -266,17 +267,21 @@ sr_status hip_fail(hipError_t e, const char* what);
 struct LaunchGuard {
   const char* name;
   hipStream_t stream;
-  int slot;
+  int slot;                      // >= 0: this launch is timed
+  hipEvent_t ev_start, ev_stop;  // recorded by the dispatch itself (no separate event packets)
   LaunchGuard(const char* n, hipStream_t s);
-  sr_status done();  // records the closing event (if any) and checks the launch
+  sr_status done();  // counts the timed launch and checks the launch
 };
 
 }  // namespace sr
 
-#define SR_LAUNCH(NAME, KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                 \
-  do {                                                                            \
-    ::sr::LaunchGuard _g((NAME), (STREAM));                                       \
-    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);          \
-    sr_status _st = _g.done();                                                    \
-    if (_st != SR_OK) return _st;                                                 \
+#define SR_LAUNCH(NAME, KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                                      \
+  do {                                                                                                 \
+    ::sr::LaunchGuard _g((NAME), (STREAM));                                                            \
+    if (_g.slot >= 0)                                                                                  \
+      hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, _g.ev_start, _g.ev_stop, 0, __VA_ARGS__); \
+    else                                                                                               \
+      hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                             \
+    sr_status _st = _g.done();                                                                         \
+    if (_st != SR_OK) return _st;                                                                      \
   } while (0)
