@@ -41,6 +41,85 @@ __global__ __launch_bounds__(256) void k_clip_ln(const T* __restrict__ hidden, c
   const size_t row = (size_t)b * d;
   float scale = 0.f;
   bool act = corr != nullptr && (active == nullptr || active[b] != 0);
+  if constexpr (sizeof(T) == 2) {
+    if (d % 8 == 0 && d <= 256 * CLN_MAXE && blockDim.x == 256) {
+      // bf16 rows: 8 consecutive elements per 16-byte access, the row in registers; one reduction for
+      // ||corr||^2, sum h and sum corr (the mean of x = h + s corr follows from them), one for the
+      // centred squares
+      constexpr int NCK = CLN_MAXE / 8;        // 8-element chunks per thread
+      float hv[NCK][8], cv[NCK][8];
+      __shared__ float red3[8][3];
+      float ss = 0.f, sh = 0.f, sc = 0.f;
+#pragma unroll
+      for (int k = 0; k < NCK; ++k) {
+        const int i0 = (tid + k * 256) * 8;
+        if (i0 < d) {
+          const u32x4 hw = *(const u32x4*)(hidden + row + i0);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hv[k][e] = bf2f((e & 1) ? (hw[e >> 1] >> 16) : (hw[e >> 1] & 0xffffu));
+          if (act) {
+            const f32x4 c0 = *(const f32x4*)(corr + row + i0), c1 = *(const f32x4*)(corr + row + i0 + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { cv[k][e] = c0[e]; cv[k][e + 4] = c1[e]; }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) cv[k][e] = 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hv[k][e] = cv[k][e] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { ss += cv[k][e] * cv[k][e]; sh += hv[k][e]; sc += cv[k][e]; }
+      }
+      ss = warp_sum(ss); sh = warp_sum(sh); sc = warp_sum(sc);
+      if ((tid & 63) == 0) { red3[tid >> 6][0] = ss; red3[tid >> 6][1] = sh; red3[tid >> 6][2] = sc; }
+      __syncthreads();
+      float tss = 0.f, tsh = 0.f, tsc = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) { tss += red3[w][0]; tsh += red3[w][1]; tsc += red3[w][2]; }
+      if (act) {
+        const float nrm = sqrtf(tss);
+        scale = nrm > 0.f ? fminf(1.f, clip_norm / nrm) : 0.f;
+      }
+      const float mean = (tsh + scale * tsc) / (float)d;
+      float q = 0.f;
+#pragma unroll
+      for (int k = 0; k < NCK; ++k) {
+        const int i0 = (tid + k * 256) * 8;
+        if (i0 < d) {
+          f32x4 x0, x1;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            hv[k][e] = hv[k][e] + (act ? scale * cv[k][e] : 0.f);
+            const float v = hv[k][e] - mean;
+            q += v * v;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) { x0[e] = hv[k][e]; x1[e] = hv[k][e + 4]; }
+          *(f32x4*)(x_out + row + i0) = x0;
+          *(f32x4*)(x_out + row + i0 + 4) = x1;
+        }
+      }
+      q = warp_sum(q);
+      if ((tid & 63) == 0) red3[4 + (tid >> 6)][0] = q;
+      __syncthreads();
+      const float var = (red3[4][0] + red3[5][0] + red3[6][0] + red3[7][0]) / (float)d;
+      const float rs = 1.f / sqrtf(var + eps);
+#pragma unroll
+      for (int k = 0; k < NCK; ++k) {
+        const int i0 = (tid + k * 256) * 8;
+        if (i0 < d) {
+          u32x4 nw;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            nw[e] = (uint32_t)f2bf((hv[k][2 * e] - mean) * rs) | ((uint32_t)f2bf((hv[k][2 * e + 1] - mean) * rs) << 16);
+          *(u32x4*)(n_out + row + i0) = nw;
+        }
+      }
+      return;
+    }
+  }
   if (d <= 256 * CLN_MAXE && blockDim.x == 256) {
     // the row stays in registers: one round trip for the loads, the same sums in the same order
     float hv[CLN_MAXE], cv[CLN_MAXE];
