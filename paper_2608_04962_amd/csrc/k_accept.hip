@@ -458,7 +458,7 @@ __device__ void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, flo
 // Nucleus cut of the current row (after row_stats_nuc): membership fields of sm, sm.S = the nucleus mass
 // and sm.nk_margin. Whole block.
 template <typename T>
-__device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float invtau, float top_p) {
+__device__ __attribute__((noinline)) void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float invtau, float top_p) {
   // the first digit's histogram comes from row_stats_nuc
   const int tid = threadIdx.x, wave = tid >> 6;
   constexpr bool BF = sizeof(T) == 2;
@@ -518,10 +518,190 @@ __device__ void nucleus(AccSmem& sm, const T* __restrict__ row, int V, float inv
   __syncthreads();
 }
 
+// Boundary-bin tallies of the fused nucleus pass (bf16 rows): per chunk and second key digit, the summed
+// weight (fp32; every cell is updated by the one wave that owns its chunk) and the token count (two 16-bit
+// counts per word; a chunk holds at most 512 tokens).
+constexpr int NUC_D2 = 32;                   // values of the second digit of a bf16 key (bits 16..20)
+struct NucBins {
+  float bm[ACC_MAX_CHUNKS * NUC_D2];
+  uint32_t bc[ACC_MAX_CHUNKS * NUC_D2 / 2];
+};
+__device__ __forceinline__ int nuc_bcount(const NucBins& nb, int c, int d) {
+  return (int)((nb.bc[c * (NUC_D2 / 2) + (d >> 1)] >> (16 * (d & 1))) & 0xffffu);
+}
+
+// The nucleus cut of a bf16 row and its masked chunk sums in one pass over the row (after row_stats_nuc),
+// in place of nucleus + nuc_masked_sums. A bf16 key is fixed by its top 16 bits: the first digit (bits
+// 21..31) comes from row_stats_nuc's histogram, the second (bits 16..20) from this pass. Knowing the first
+// digit's cut bin b1, the pass sums per chunk the weights of the tokens above b1 (members whatever the
+// second digit), and tallies the tokens of bin b1 by chunk and second digit (weight and count) beside the
+// second digit's histogram. Once the second digit d2 is found, a chunk's nucleus sum is its sum above b1,
+// plus its bin-b1 weight of digits above d2, plus its kept tokens of the cut key (all of one weight).
+// The cut itself (key, id cut, mass, margin) is computed exactly as nucleus computes it.
+__device__ __attribute__((noinline)) void nucleus_bf16(AccSmem& sm, NucBins& nb, const bf16_t* __restrict__ row, int V, float invtau,
+                             float top_p) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (V + ACC_CH - 1) / ACC_CH;
+  // total mass, target and the first digit's cut bin, from row_stats_nuc's histogram
+  if (wave == 0) {
+    unsigned long long ls = 0;
+    for (int b = lane; b < NUC_NB; b += 64) ls += sm.nh[b];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ls += __shfl_xor(ls, o, 64);
+    if (lane == 0) sm.nk_above = ls;          // stash the total
+  }
+  __syncthreads();
+  const unsigned long long total = sm.nk_above;
+  const unsigned long long target = (unsigned long long)ceil((double)top_p * (double)total);
+  __syncthreads();
+  if (wave == 0) nuc_find(sm, NUC_NB, 0ull, target);
+  __syncthreads();
+  const uint32_t b1 = (uint32_t)sm.nk_b;
+  const unsigned long long above1 = sm.nk_above;
+  for (int i = tid; i < nch * NUC_D2; i += ACC_NT) nb.bm[i] = 0.f;
+  for (int i = tid; i < nch * (NUC_D2 / 2); i += ACC_NT) nb.bc[i] = 0u;
+  __syncthreads();                            // every thread has read nk_b / nk_above before nh is reused
+  for (int i = tid; i < NUC_D2; i += ACC_NT) sm.nh[i] = 0ull;
+  __syncthreads();
+  const float M = sm.M;
+  constexpr int GRP = RowLoad<bf16_t>::GROUP;
+  for (int c0 = wave * GRP; c0 < nch; c0 += ACC_NW * GRP) {
+    RowLoad<bf16_t>::Raw w[GRP];
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) {
+      const int base = (c0 + gi) * ACC_CH + lane * 8;
+      w[gi] = (c0 + gi < nch && base < V) ? RowLoad<bf16_t>::raw(row + base) : RowLoad<bf16_t>::ninf();
+    }
+    float a[GRP];                              // this lane's weight above bin b1, per chunk
+#pragma unroll
+    for (int gi = 0; gi < GRP; ++gi) {
+      a[gi] = 0.f;
+      const int c = min(c0 + gi, nch - 1);     // past the row every token is -inf and tallies nothing
+      float x[8];
+      RowLoad<bf16_t>::unpack(w[gi], x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t k = acc_key(x[e]);
+        const uint32_t d1 = k >> 21;
+        if (x[e] != -INFINITY && d1 >= b1) {
+          const float wt = tilt(x[e], invtau, M);
+          if (d1 > b1) {
+            a[gi] += wt;
+          } else {
+            const int d = (int)((k >> 16) & (NUC_D2 - 1));
+            atomicAdd(&nb.bm[c * NUC_D2 + d], wt);
+            atomicAdd(&nb.bc[c * (NUC_D2 / 2) + (d >> 1)], 1u << (16 * (d & 1)));
+            atomicAdd(&sm.nh[d], nuc_fixed(wt));
+          }
+        }
+      }
+    }
+    int j;
+    const float sc = wave_sum_scatter<GRP>(a, j);
+    if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) sm.csum[c0 + j] = (double)sc;
+  }
+  __syncthreads();
+  if (wave == 0) nuc_find(sm, NUC_D2, above1, target);
+  __syncthreads();
+  const int d2 = sm.nk_b;
+  const unsigned long long above = sm.nk_above, bin_mass = sm.nk_bin;
+  uint32_t prefix = (b1 << 21) | ((uint32_t)d2 << 16);
+  // a bf16 value widened to fp32 has 16 zero low bits: the key's low bits are all zero (positive) or all one
+  // (negative)
+  if (!(prefix & 0x80000000u)) prefix |= 0xffffu;
+  const uint32_t u = (prefix & 0x80000000u) ? (prefix & 0x7fffffffu) : ~prefix;
+  const float xk = __uint_as_float(u);
+  const float wk = tilt(xk, invtau, M);       // the weight of every token with the cut key
+  const unsigned long long q = nuc_fixed(wk);
+  const unsigned long long n_tie = q > 0 ? bin_mass / q : 1;
+  const unsigned long long need = q > 0 ? (target - above + q - 1) / q : n_tie;
+  const unsigned long long kt = need < n_tie ? need : n_tie;
+  if (tid == 0) {
+    sm.nk_key = prefix;
+    sm.nk_idcut = 0x7fffffff;
+    const double bl = (double)(above + (kt - 1) * q), bh = bl + (double)q, tg = (double)top_p * (double)total;
+    sm.nk_margin = fmin(tg - bl, bh - tg) / (double)total;
+    sm.S = (double)(above + kt * q) / NUC_FP;
+  }
+  // chunk holding the last kept token of the cut key and the kept ones before it, from the tallies (wave 0)
+  int cstar = nch, cbefore = 0;
+  if (kt < n_tie && wave == 0) {
+    constexpr int CPL = ACC_MAX_CHUNKS / 64;
+    const int want = (int)kt;
+    int cnt[CPL], ls = 0;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int c = lane * CPL + i;
+      cnt[i] = c < nch ? nuc_bcount(nb, c, d2) : 0;
+      ls += cnt[i];
+    }
+    int incl = ls;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    int before = incl - ls, cs = -1, cb = 0;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (cs < 0 && before < want && want <= before + cnt[i]) { cs = lane * CPL + i; cb = before; }
+      before += cnt[i];
+    }
+    const unsigned long long bal = __ballot(cs >= 0);
+    const int owner = bal ? __ffsll((long long)bal) - 1 : 0;
+    cstar = max(0, __shfl(cs, owner, 64));
+    cbefore = __shfl(cb, owner, 64);
+    // the id of the want-th token of the cut key: scan chunk cstar, 8 tokens per lane
+    const int base = cstar * ACC_CH + lane * 8;
+    float x[8];
+    int n = 0;
+    if (base < V) {
+      RowLoad<bf16_t>::load8(row + base, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) n += (x[e] != -INFINITY && acc_key(x[e]) == prefix) ? 1 : 0;
+    }
+    int li = n;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(li, o, 64);
+      if (lane >= o) li += t;
+    }
+    int cum = cbefore + li - n, id = -1;
+    if (base < V) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (x[e] != -INFINITY && acc_key(x[e]) == prefix) {
+          ++cum;
+          if (cum == want && id < 0) id = base + e;
+        }
+      }
+    }
+    const unsigned long long b2 = __ballot(id >= 0);
+    const int idv = __shfl(id, b2 ? __ffsll((long long)b2) - 1 : 0, 64);
+    if (lane == 0) {
+      if (b2) sm.nk_idcut = idv;
+      sm.nk_b = cstar;                          // handed to the masked sums below
+      sm.nk_bin = (unsigned long long)cbefore;
+    }
+  }
+  __syncthreads();
+  if (kt < n_tie) { cstar = sm.nk_b; cbefore = (int)sm.nk_bin; }
+  // masked chunk sums: above b1, plus bin b1's digits above d2, plus the kept tokens of the cut key
+  for (int c = tid; c < nch; c += ACC_NT) {
+    double sum = sm.csum[c];
+    for (int d = d2 + 1; d < NUC_D2; ++d) sum += (double)nb.bm[c * NUC_D2 + d];
+    const int nt = nuc_bcount(nb, c, d2);
+    const int kept = c < cstar ? nt : (c == cstar ? (int)kt - cbefore : 0);
+    sm.csum[c] = sum + (double)kept * (double)wk;
+  }
+  if (tid == 0) sm.nk_on = 1;
+  __syncthreads();
+}
+
 // chunk sums restricted to the nucleus (for the terminal draws), relative to the chunks' reference
 // maxima; the same chunk groups and exchanges as row_stats
 template <typename T>
-__device__ void nuc_masked_sums(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
+__device__ __attribute__((noinline)) void nuc_masked_sums(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
   constexpr int GRP = RowLoad<T>::GROUP;
@@ -803,6 +983,17 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   int u = 0;
   const float Ufin = u_fin[b];
   const int nch = (V + ACC_CH - 1) / ACC_CH;
+  // nucleus cut of a row and its masked chunk sums: one fused pass for bf16 rows, two (plus the tie count
+  // when the cut splits a key) for fp32 rows, whose keys take three digits
+  auto nuc_cut = [&](const T* r) __attribute__((always_inline)) {
+    if constexpr (NUC && sizeof(T) == 2) {
+      __shared__ NucBins nb;
+      nucleus_bf16(sm, nb, r, V, invtau, top_p);
+    } else {
+      nucleus<T>(sm, r, V, invtau, top_p);
+      nuc_masked_sums<T>(sm, r, V, invtau);
+    }
+  };
   while (true) {
     const T* row = base + (size_t)u * V;
     // the node's children in node order (ballot compaction) and, for the plain walk, the chunks that
@@ -832,10 +1023,9 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     const int m = sm.nkid;
     if constexpr (NUC) {
       row_stats_nuc<T>(sm, row, V, invtau);
-      nucleus<T>(sm, row, V, invtau, top_p);
+      nuc_cut(row);                             // and the chunk sums over the nucleus
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
-      nuc_masked_sums<T>(sm, row, V, invtau);   // chunk sums over the nucleus; outside_mass sums them to S
-      outside_mass<T, NUC>(sm, row, V, invtau, m);
+      outside_mass<T, NUC>(sm, row, V, invtau, m);   // sums the masked chunk sums to S
     } else {
       row_stats<T>(sm, row, V, invtau, m);     // with the children's chunks and logits
     }
@@ -924,9 +1114,8 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     const T* lrow = base + (size_t)c * V;
     if constexpr (NUC) {
       row_stats_nuc<T>(sm, lrow, V, invtau);
-      nucleus<T>(sm, lrow, V, invtau, top_p);
+      nuc_cut(lrow);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
-      nuc_masked_sums<T>(sm, lrow, V, invtau);
     } else {
       row_stats<T>(sm, lrow, V, invtau, 0);
     }
