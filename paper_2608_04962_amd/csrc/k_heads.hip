@@ -844,6 +844,15 @@ __global__ __launch_bounds__(TOPM_NT) void k_topm_grouped(const float* __restric
 // The wave holds C_u across its lanes, so each draw's float64 weights, their sum and the cumulative
 // weights in C_u's order are computed in parallel.
 constexpr int TB_NT = 1024;           // 16 waves: one node with children per wave at a time
+
+// a float64 moved across the lanes of each 16-lane row by the DPP control CTRL (lanes whose source lies
+// outside the row read 0)
+template <int CTRL>
+__device__ __forceinline__ double dpp0_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xf, 0xf, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xf, 0xf, true);
+  return __hiloint2double(hi, lo);
+}
 __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict__ top_id,
                                                      const float* __restrict__ top_val, int H, int M, int T,
                                                      const int32_t* __restrict__ parents,
@@ -872,16 +881,20 @@ __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict_
     return;
   }
   if (tid == 0) { tok_b[0] = root_token[b]; cl_b[0] = 0.f; }
-  // one wave per node with children; lane i holds candidates i and i + 64 of C_u
-  for (int u = wave; u < T; u += TB_NT / 64) {
-    const int m = t.nkids[u];
-    if (m == 0) continue;                                      // uniform per wave
+  // one wave per node with children; lane i holds candidates i and i + 64 of C_u (the second only when
+  // m_u > 64: with fewer candidates every second slot is empty and its weights, sums and ballots are zero)
+  // NS = 0: at most 16 candidates, all in the first 16-lane row: the max, the prefix sums and the total
+  // move by DPP within that row. The sums are the same additions in the same order as the wave-wide scan
+  // (whose further steps only add zeros there), so the draws are identical.
+  auto draws = [&](int u, int m, auto ns_) __attribute__((always_inline)) {
+    constexpr bool R16 = decltype(ns_)::value == 0;
+    constexpr int NS = R16 ? 1 : decltype(ns_)::value;
     const int k = min(t.depth[u] + 1, H);                      // proposing head, 1-based
     const size_t rbase = ((size_t)b * H + (k - 1)) * M;
-    double l[2];
-    bool live[2];
+    double l[NS];
+    bool live[NS];
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
+    for (int s2 = 0; s2 < NS; ++s2) {
       const int i = lane + 64 * s2;
       live[s2] = i < m;
       l[s2] = live[s2] ? (double)top_val[rbase + i] : -INFINITY;
@@ -890,35 +903,61 @@ __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict_
     for (int j = 0; j < m; ++j) {
       while (t.parent[c] != u) ++c;                            // j-th child of u in index order
       // weights exp(l - max over the remaining candidates), float64, in C_u's order
-      const double mx = wave_max_f64(fmax(live[0] ? l[0] : -INFINITY, live[1] ? l[1] : -INFINITY));
-      double w[2];
+      double lm = -INFINITY;
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) w[s2] = live[s2] ? exp(l[s2] - mx) : 0.0;
+      for (int s2 = 0; s2 < NS; ++s2) lm = fmax(lm, live[s2] ? l[s2] : -INFINITY);
+      double mx;
+      if constexpr (R16) {
+        mx = fmax(lm, dpp_f64<0xb1>(lm));         // quad_perm [1,0,3,2]
+        mx = fmax(mx, dpp_f64<0x4e>(mx));         // quad_perm [2,3,0,1]
+        mx = fmax(mx, dpp_f64<0x141>(mx));        // row_half_mirror
+        mx = fmax(mx, dpp_f64<0x140>(mx));        // row_mirror
+      } else {
+        mx = wave_max_f64(lm);
+      }
+      double w[NS];
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) w[s2] = live[s2] ? exp(l[s2] - mx) : 0.0;
       // inclusive prefix sums over candidates 0..63, then 64..127
-      double cum[2];
+      double cum[NS];
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
+      for (int s2 = 0; s2 < NS; ++s2) {
         double v = w[s2];
+        if constexpr (R16) {
+          v += dpp0_f64<0x111>(v);                 // row_shr:1, 2, 4, 8
+          v += dpp0_f64<0x112>(v);
+          v += dpp0_f64<0x114>(v);
+          v += dpp0_f64<0x118>(v);
+        } else {
 #pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const double y = __shfl_up(v, o, 64);
-          if (lane >= o) v += y;
+          for (int o = 1; o < 64; o <<= 1) {
+            const double y = __shfl_up(v, o, 64);
+            if (lane >= o) v += y;
+          }
         }
         cum[s2] = v;
       }
-      const double tot0 = __shfl(cum[0], 63, 64);
-      cum[1] += tot0;
-      const double S = __shfl(cum[1], 63, 64);
+      if constexpr (NS == 2) cum[1] += __shfl(cum[0], 63, 64);
+      double S;
+      if constexpr (R16)
+        S = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(cum[0]), 15),
+                             __builtin_amdgcn_readlane(__double2loint(cum[0]), 15));
+      else
+        S = __shfl(cum[NS - 1], 63, 64);
       const double target = (double)u_tree[(size_t)b * T + c] * S;
       // first candidate whose cumulative weight exceeds the target; the last live one on rounding
-      const unsigned long long hit0 = __ballot(live[0] && target < cum[0]);
-      const unsigned long long hit1 = __ballot(live[1] && target < cum[1]);
-      int pick;
-      if (hit0) pick = __ffsll((long long)hit0) - 1;
-      else if (hit1) pick = 64 + __ffsll((long long)hit1) - 1;
-      else {
-        const unsigned long long l1 = __ballot(live[1]), l0 = __ballot(live[0]);
-        pick = l1 ? 64 + 63 - __clzll((long long)l1) : 63 - __clzll((long long)l0);
+      int pick = -1;
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) {
+        const unsigned long long hit = __ballot(live[s2] && target < cum[s2]);
+        if (pick < 0 && hit) pick = 64 * s2 + __ffsll((long long)hit) - 1;
+      }
+      if (pick < 0) {
+#pragma unroll
+        for (int s2 = NS - 1; s2 >= 0; --s2) {
+          const unsigned long long lv = __ballot(live[s2]);
+          if (pick < 0 && lv) pick = 64 * s2 + 63 - __clzll((long long)lv);
+        }
       }
       if (lane == (pick & 63)) live[pick >> 6] = false;
       if (lane == 0) {
@@ -927,6 +966,13 @@ __global__ __launch_bounds__(TB_NT) void k_tree_build(const int32_t* __restrict_
       }
       ++c;
     }
+  };
+  for (int u = wave; u < T; u += TB_NT / 64) {
+    const int m = t.nkids[u];
+    if (m == 0) continue;                                      // uniform per wave
+    if (m > 64) draws(u, m, std::integral_constant<int, 2>{});
+    else if (m > 16) draws(u, m, std::integral_constant<int, 1>{});
+    else draws(u, m, std::integral_constant<int, 0>{});
   }
 }
 
