@@ -13,36 +13,43 @@ __device__ __forceinline__ uint32_t fkey(float f) {
 constexpr int TOPM_NT = 512;
 constexpr int TOPM_BINS = 2048;
 
+// Inclusive prefix sum of per-thread counts over the block, and the block total: within each wave by DPP
+// (row shifts 1, 2, 4, 8, then the three lower rows' totals), across the waves through sh (one entry per
+// wave) and one barrier. Integer sums: the same result in any order. Ends with a barrier, so sh may be
+// reused at once.
+__device__ inline int block_incl_scan(int v, int* sh, int* total) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int NWV = TOPM_NT / 64;
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true);   // row_shr:1 (lanes past the row read 0)
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true);   // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, true);   // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, true);   // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+            r2 = __builtin_amdgcn_readlane(v, 47), r3 = __builtin_amdgcn_readlane(v, 63);
+  const int row = lane >> 4;
+  v += (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
+  if (lane == 0) sh[wave] = r0 + r1 + r2 + r3;
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NWV; ++w) {
+    const int t = sh[w];
+    before += w < wave ? t : 0;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + v;
+}
 // Suffix (exclusive, from the top) scan of per-thread counts over the block.
 __device__ inline int block_suffix_excl(int v, int* sh) {
-  const int tid = threadIdx.x;
-  sh[tid] = v;
-  __syncthreads();
-  for (int o = 1; o < TOPM_NT; o <<= 1) {
-    int add = (tid + o < TOPM_NT) ? sh[tid + o] : 0;
-    __syncthreads();
-    sh[tid] += add;
-    __syncthreads();
-  }
-  int incl = sh[tid];
-  __syncthreads();
-  return incl - v;
+  int total;
+  const int incl = block_incl_scan(v, sh, &total);
+  return total - incl;
 }
 // Prefix (exclusive) scan of per-thread counts; also returns the total.
 __device__ inline int block_prefix_excl(int v, int* sh, int* total) {
-  const int tid = threadIdx.x;
-  sh[tid] = v;
-  __syncthreads();
-  for (int o = 1; o < TOPM_NT; o <<= 1) {
-    int add = (tid >= o) ? sh[tid - o] : 0;
-    __syncthreads();
-    sh[tid] += add;
-    __syncthreads();
-  }
-  int incl = sh[tid];
-  *total = sh[TOPM_NT - 1];
-  __syncthreads();
-  return incl - v;
+  return block_incl_scan(v, sh, total) - v;
 }
 
 // Radix select over n order-preserving keys: after it, st.prefix is the key K* of the k-th largest
