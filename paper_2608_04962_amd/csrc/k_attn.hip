@@ -532,8 +532,9 @@ struct DmaGeom {
   static constexpr int TILE = ATT_KT * ROWB;           // bytes of a K (or raw V) tile
   static constexpr int BLK = TILE / 1024;              // DMA blocks per tile, each of K and V
   static constexpr int CITEMS = TILE / 16;             // 16-byte chunks of a V tile (conversion items)
-  static constexpr int CPL = CITEMS / 64;                // V chunks per lane of the converting (DMA) wave
-  static_assert(CITEMS % 64 == 0, "tile split");
+  static constexpr int CPL = CITEMS / 64;                // V chunks of a tile per lane of one wave
+  static constexpr int CD = CPL - (ATT_NW - 1);          // converted per lane by the DMA wave; one by each other wave
+  static_assert(CITEMS % 64 == 0 && CD >= 1, "tile split");
   static_assert(2 * BLK <= 63, "one tile of DMA per wave must fit the vmcnt counter");
   static_assert(KPB % 4 == 0, "a DMA block holds whole 4-key groups");
 };
@@ -618,11 +619,11 @@ __device__ __forceinline__ void attn_item_dma(
   for (int i = 0; i < NDT; ++i) o[i] = (f32x16){};
   float m_run = -INFINITY, l_run = 0.f;
   // Roles. A row group holds at most ATT_ROWS - 32 rows (attn_plan), so wave n_act has no query rows: it
-  // issues all of the DMA, pacing itself on the memory system, and converts every V tile to fp16. It runs
-  // its own loop (the same barriers), so its conversion registers never share the compute waves' code.
-  // Measured per 64-key tile at the 7B shape: with the seven compute waves converting V, the second wave of
-  // each SIMD took 1.45k cycles for conversion and max, 2.3k for exponentials and next scores, 0.66k for
-  // P V, while the DMA wave waited 2.9k of its 4.6k at the barrier.
+  // issues all of the DMA, pacing itself on the memory system, and converts most of every V tile to fp16;
+  // each other wave converts one 16-byte chunk per lane of it. The DMA wave runs its own loop (the same
+  // barriers), so its conversion registers never share the compute waves' code. Measured per 64-key tile
+  // at the 7B shape (about 4.4k cycles): issuing a tile's 32 transfers took the DMA wave about 1.9k cycles
+  // and converting all of its V about 2.0k; the second compute wave of each SIMD about 3.3-3.5k.
   const int n_act = min(ATT_NW - 1, (rend - rg * group_rows + 31) / 32);
   const bool wave_active = wave < n_act && !bad;
   const bool dma_wave = wave == n_act;
@@ -710,35 +711,36 @@ __device__ __forceinline__ void attn_item_dma(
   // converts (two 16-bit lanes per register): an item is recomputed with fp32 V when that exceeds 65280
   // (pattern 0x477f; inf and NaN included) or when the item's largest |v| is below 2^-6 (pattern 0x3c80),
   // where 2^-24 would no longer be negligible against the scale of V.
-  u32x4 cw[G::CPL];
+  // The DMA wave converts chunks lane + 64 k (k < CD) of a tile; every other wave converts one chunk,
+  // (CD + its index among the other waves) * 64 + lane, beside its own work: the DMA wave's issue is paced
+  // by the memory system and takes a large part of a tile's time.
   u16x2 vmag_hi = {0, 0};
+  auto conv_chunk = [&](const u32x4& x, unsigned char* dst) __attribute__((always_inline)) {
+    // two values per instruction, rounding toward zero: exact for every value in fp16's normal range,
+    // within one subnormal step (2^-24) below it; out-of-range items are recomputed anyway
+    u32x4 h;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      h[w] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(__uint_as_float(x[w] << 16),
+                                                                     __uint_as_float(x[w] & 0xffff0000u)));
+      vmag_hi = __builtin_elementwise_max(vmag_hi, __builtin_bit_cast(u16x2, x[w] & 0x7fff7fffu));
+    }
+    *(u32x4*)dst = h;
+  };
+  u32x4 cw[G::CD];
   auto conv_load = [&](const unsigned char* v) __attribute__((always_inline)) {
     int ln = lane;
     asm volatile("" : "+v"(ln));                  // addresses are not hoisted out of the tile loop
 #pragma unroll
-    for (int k = 0; k < G::CPL; ++k) cw[k] = *(const u32x4*)(v + (ln + k * 64) * 16);
+    for (int k = 0; k < G::CD; ++k) cw[k] = *(const u32x4*)(v + (ln + k * 64) * 16);
   };
   auto conv_store = [&](unsigned char* v) __attribute__((always_inline)) {
     int ln = lane;
     asm volatile("" : "+v"(ln));
 #pragma unroll
-    for (int k = 0; k < G::CPL; ++k) {
-      const int it = ln + k * 64;
-      {
-        // two values per instruction, rounding toward zero: exact for every value in fp16's normal range,
-        // within one subnormal step (2^-24) below it; out-of-range items are recomputed anyway
-        u32x4 h;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const uint32_t x = cw[k][w];
-          h[w] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(__uint_as_float(x << 16),
-                                                                         __uint_as_float(x & 0xffff0000u)));
-          vmag_hi = __builtin_elementwise_max(vmag_hi, __builtin_bit_cast(u16x2, x & 0x7fff7fffu));
-        }
-        *(u32x4*)(v + it * 16) = h;
-      }
-    }
+    for (int k = 0; k < G::CD; ++k) conv_chunk(cw[k], v + (ln + k * 64) * 16);
   };
+  const int help_off = ((G::CD + (wave < n_act ? wave : wave - 1)) * 64 + lane) * 16;   // other waves' chunk
   // scores S^T = K Q^T of the tile in ks
   auto qk = [&](const unsigned char* ks, f32x16 (&s)[2]) {
     s[0] = s[1] = (f32x16){};
@@ -781,8 +783,9 @@ __device__ __forceinline__ void attn_item_dma(
     }
   };
   // from a lane's max of a tile's (masked) scores: the row max, the new reference max and the accumulator
-  // rescale. The reference max moves only when the tile max exceeds it by more than 2^8, so P stays in
-  // [0, 256] (exact in fp16 up to rounding) and the accumulator is rarely rescaled.
+  // rescale. The reference max moves only when the tile max exceeds it by more than 2^8, so the accumulator
+  // is rarely rescaled. Run for the first tile and for a tile whose weights outgrow the reference
+  // (finish_rest).
   auto commit_max = [&](float mx) {
     mx = max_halves(mx);
     const float tmax = mx * scale_log2;
@@ -806,13 +809,12 @@ __device__ __forceinline__ void attn_item_dma(
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
     commit_max(mx);
   };
-  // exponentials of tile i (scores s), computed in one basic block with the scores of the next tile (K in
-  // nks, into sn), then O^T += V^T P^T with V of tile i (vs); with `next`, the mask and max of the next
-  // tile's scores follow, the max spread over the P V MFMAs (the matrix core works while the vector ALU
-  // reduces), and the rescale after them
+  // exponentials of tile i (scores s) against the current reference max, computed in one basic block with
+  // the scores of the next tile (K in nks, into sn), then O^T += V^T P^T with V of tile i (vs); with `next`,
+  // the mask of the next tile's scores (partial or tree tiles)
   auto finish_rest = [&](int i, f32x16 (&s)[2], const unsigned char* vs, const unsigned char* nks, f32x16 (&sn)[2],
                          bool next) {
-    const float m_use = f_muse, alpha = f_alpha;
+    float m_use = f_muse;
     // From here on one basic block, laid out by hand with scheduling fences: each step issues the
     // K fragment reads one step ahead, two score MFMAs of the next tile and 32/NQF of this tile's
     // exponentials (the matrix core works while the vector ALU exponentiates); then the P V MFMAs
@@ -820,6 +822,16 @@ __device__ __forceinline__ void attn_item_dma(
     constexpr int EPQ = 32 / NQF;                 // exponentials per score step
     f16x8 pf[2][2];
     float psum = 0.f;
+    // weights of scores e, e+1 of this tile into pf; the row sum takes the fp16 weights the P V product
+    // uses, in fp32 (v_dot2_f32_f16)
+    auto exp_pair = [&](int e) __attribute__((always_inline)) {
+      const int kt = e >> 4, r = e & 15;
+      const _Float16 h0 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
+      const _Float16 h1 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r + 1], scale_log2, -m_use));
+      pf[kt][r >> 3][r & 7] = h0;
+      pf[kt][r >> 3][(r & 7) + 1] = h1;
+      psum = __builtin_amdgcn_fdot2((f16x2){h0, h1}, (f16x2){(_Float16)1.f, (_Float16)1.f}, psum, false);
+    };
     u32x4 kf[2][2];
     auto kread = [&](int kq, u32x4 (&dst)[2]) {
 #pragma unroll
@@ -838,18 +850,29 @@ __device__ __forceinline__ void attn_item_dma(
         sn[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kq & 1][kt]),
                                                          __builtin_bit_cast(bf16x8, qf[kq]), sn[kt], 0, 0, 0);
 #pragma unroll
-      for (int e = kq * EPQ; e < (kq + 1) * EPQ; e += 2) {
-        const int kt = e >> 4, r = e & 15;
-        const _Float16 h0 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], scale_log2, -m_use));
-        const _Float16 h1 = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r + 1], scale_log2, -m_use));
-        pf[kt][r >> 3][r & 7] = h0;
-        pf[kt][r >> 3][(r & 7) + 1] = h1;
-        // the row sum takes the fp16 weights the P V product uses, in fp32 (v_dot2_f32_f16)
-        psum = __builtin_amdgcn_fdot2((f16x2){h0, h1}, (f16x2){(_Float16)1.f, (_Float16)1.f}, psum, false);
-      }
+      for (int e = kq * EPQ; e < (kq + 1) * EPQ; e += 2) exp_pair(e);
       __builtin_amdgcn_sched_barrier(0);
     }
-    l_run = l_run * alpha + psum;
+    // The reference max is lazy: no tile max is taken while every lane's weights stay small. A tile whose
+    // half-row weights add up past 2^14 (or overflow) moves the reference to its own max (the row max and
+    // the accumulator rescale as for the first tile) and is weighted again; weights below 2^14 are exact in
+    // fp16 up to its rounding, like those below 2^8.
+    if (__ballot(!(psum <= 16384.f)) != 0) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+      const float a0 = f_alpha;
+      commit_max(mx);
+      f_alpha *= a0;
+      m_use = f_muse;
+      psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 32; e += 2) exp_pair(e);
+    }
+    l_run = l_run * f_alpha + psum;
+    f_alpha = 1.f;
     constexpr int NPV = 4 * NDT;                  // P V MFMAs per tile
     f16x8 vf[3];
     // V^T fragment (dims dt*32 + lane%32; keys of k-slot 8*half + j: 16 kq + 8 (j/4) + 4 half + j%4) as two
@@ -870,8 +893,6 @@ __device__ __forceinline__ void attn_item_dma(
       return (f16x8){part[0][0], part[0][1], part[0][2], part[0][3], part[1][0], part[1][1], part[1][2], part[1][3]};
     };
     if (next && !tile_full(i + 1)) mask_tile(i + 1, sn);
-    constexpr int MPJ = 32 / NPV;               // next-tile scores maxed per P V MFMA
-    float mx = -INFINITY;
     vf[0] = vread(0);
     vf[1] = vread(1);
 #pragma unroll
@@ -879,11 +900,8 @@ __device__ __forceinline__ void attn_item_dma(
       if (j + 2 < NPV) vf[(j + 2) % 3] = vread(j + 2);
       const int kt = j / (2 * NDT), kq = (j / NDT) & 1, dt = j % NDT;
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[j % 3], pf[kt][kq], o[dt], 0, 0, 0);
-#pragma unroll
-      for (int e = j * MPJ; e < (j + 1) * MPJ; ++e) mx = fmaxf(mx, sn[e >> 4][e & 15]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (next) commit_max(mx);
   };
 
   // ---- pipeline. Compute waves, step(i): wait for tile i+1, then finish tile i while computing the scores of
@@ -894,8 +912,13 @@ __device__ __forceinline__ void attn_item_dma(
   auto step = [&](int i, int si, f32x16 (&s)[2], f32x16 (&sn)[2]) {
     const int sn_ = (si + 1) & 3;
     attn_sync<D>(false, false);
+    const bool cvn = i + 1 < n_tiles;
+    unsigned char* hc = ring[sn_] + G::TILE + help_off;   // this wave's chunk of tile i+1's V
+    u32x4 hw;
+    if (cvn) hw = *(const u32x4*)hc;
     // after the last tile the next scores come from a slot no DMA is writing and are discarded
-    if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn, i + 1 < n_tiles);
+    if (wave_active) finish_rest(i, s, ring[si] + G::TILE, ring[sn_], sn, cvn);
+    if (cvn) conv_chunk(hw, hc);
   };
   if (n_tiles > 0) {
     if (dma_wave) {
@@ -916,10 +939,15 @@ __device__ __forceinline__ void attn_item_dma(
         si = (si + 1) & 3;
       }
     } else {
-      attn_sync<D>(false, false);               // tile 0 landed and converted
-      if (wave_active) {
-        qk(ring[0], sa);
-        finish_max(0, sa);
+      attn_sync<D>(false, false);               // tile 0 landed
+      {
+        unsigned char* hc = ring[0] + G::TILE + help_off;
+        const u32x4 hw = *(const u32x4*)hc;
+        if (wave_active) {
+          qk(ring[0], sa);
+          finish_max(0, sa);
+        }
+        conv_chunk(hw, hc);
       }
       int si = 0;
       for (int i = 0; i < n_tiles; i += 2) {
@@ -939,7 +967,7 @@ __device__ __forceinline__ void attn_item_dma(
   {
     uint32_t hi = max((uint32_t)vmag_hi[0], (uint32_t)vmag_hi[1]);
     hi = (uint32_t)warp_max_i((int)hi);
-    if (dma_wave && lane == 0) atomicMax(&meta.vwide, (int)hi);
+    if (lane == 0) atomicMax(&meta.vwide, (int)hi);
     __syncthreads();
     if (threadIdx.x == 0 && n_tiles > 0 && (meta.vwide > 0x477f || meta.vwide < 0x3c80)) {
       const unsigned k = atomicAdd(redo, 1u);

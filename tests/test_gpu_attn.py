@@ -176,3 +176,35 @@ def test_bf16_v_outside_fp16_range():
     out, _ = _run_gpu(inp)
     assert np.isfinite(out).all()
     _check(inp)
+
+
+def _scale_keys(inp, traj, fn):
+    """Multiply trajectory traj's prefix K row of key position k by fn(k), and its tree K rows by fn(L + node)
+    (bf16 bits kept)."""
+    inp = dict(inp)
+    kc = synth.to_f64(inp["k_cache"], "bf16")
+    kt = synth.to_f64(inp["k_tree"], "bf16")
+    L = int(inp["ctx_len"][traj])
+    for k in range(L):
+        kc[inp["block_table"][traj, k // 16], :, k % 16, :] *= fn(k)
+    for u in range(kt.shape[1]):
+        kt[traj, u] *= fn(L + u)
+    inp["k_cache"] = synth.as_dtype(kc.astype(np.float32), "bf16")
+    inp["k_tree"] = synth.as_dtype(kt.astype(np.float32), "bf16")
+    return inp
+
+
+def test_bf16_scores_growing_falling_and_spiking():
+    """The running reference max under scores that move across tiles: keys scaled up along the context
+    (every later tile's scores above the first's), scaled down along it, one key at 12x in the middle of a
+    long context, and tree keys at 6x (the last tile holds the largest scores)."""
+    cfg = synth.scaled(synth.SHAPE_7B, B=5, T=12, depth=4, Hq=8, Hkv=2, ctx=("uniform", 1500, 3000))
+    inp = synth.attn_inputs(cfg, seed=21)
+    L = inp["ctx_len"]
+    inp = _scale_keys(inp, 0, lambda k: 0.05 + 5.0 * k / L[0])
+    inp = _scale_keys(inp, 1, lambda k: 5.05 - 5.0 * k / L[1])
+    inp = _scale_keys(inp, 2, lambda k: 12.0 if k == L[2] // 2 else 1.0)
+    inp = _scale_keys(inp, 3, lambda k: 6.0 if k >= L[3] else 1.0)
+    out, _ = _run_gpu(inp)
+    assert np.isfinite(out).all()
+    _check(inp)
