@@ -145,6 +145,25 @@ def test_tree_build_bit_exact(cfg, tie_frac):
         np.testing.assert_array_equal(cl[b], ocl[b].astype(np.float32))
 
 
+@pytest.mark.parametrize("fan", [16, 17, 64, 65, 127])
+def test_tree_build_wide_nodes(fan):
+    """A root with `fan` children and a chain below one of them: the draws of up to 16 candidates (one lane
+    row), up to 64 (one slot per lane) and more (two slots per lane), bit-exact against the oracle."""
+    T = min(fan + 1 + 3, 128)
+    par = (-1,) + (0,) * fan + tuple(range(fan, fan + T - fan - 1))
+    cfg = synth.scaled(synth.SHAPE_7B, B=6, T=T, depth=1 + (T - fan - 1), V=30000, parents=par)
+    for tie_frac in (0.0, 0.5):
+        inp = synth.head_logits_inputs(cfg, seed=7 + fan, tie_frac=tie_frac)
+        assert inp["max_children"] == fan
+        tok, cl = _gpu_tree(inp)
+        otok, ocl, mg = oracle.tree_build(inp["logits"], inp["parents"], inp["root_token"], inp["u_tree"])
+        for b in range(cfg.B):
+            if mg[b] < 1e-12:           # a draw exactly on a cumulative boundary may go either way
+                continue
+            np.testing.assert_array_equal(tok[b], otok[b])
+            np.testing.assert_array_equal(cl[b], ocl[b].astype(np.float32))
+
+
 def test_tree_build_full_vocab_rows():
     inp = synth.head_logits_inputs(synth.scaled(synth.SHAPE_7B, B=16), seed=3)
     tok, cl = _gpu_tree(inp)
