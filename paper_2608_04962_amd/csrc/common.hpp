@@ -229,10 +229,12 @@ struct TreeLds {
 template <int MAXT>
 __device__ bool tree_setup(TreeLds<MAXT>& t, const int32_t* parents_b, int T) {
   const int tid = threadIdx.x;
+  // the first parent of each thread is loaded before the barrier, in flight with the caller's own loads
+  const int p0 = tid < T ? parents_b[tid] : 0;
   if (tid == 0) t.bad = 0;
   __syncthreads();
   for (int c = tid; c < T; c += blockDim.x) {
-    int p = parents_b[c];
+    int p = c == tid ? p0 : parents_b[c];
     if ((c == 0 && p != -1) || (c > 0 && (p < 0 || p >= c))) atomicOr(&t.bad, 1);
     t.parent[c] = p;
   }
