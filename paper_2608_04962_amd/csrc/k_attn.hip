@@ -591,10 +591,8 @@ __device__ __forceinline__ void attn_item_dma(
   const int page0 = c * cp, page1 = min(pages, page0 + cp);
   const int key0 = page0 * ATT_BS, key1 = min(L, page1 * ATT_BS);
 
-  const bool bad = attn_meta<D, 2>(meta, ctx_ok, last, page0, page1, block_table + (size_t)b * max_blocks,
-                                   parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
-
-  // ---- this wave's 32 query rows: row r <-> (node t = r / G, head g*G + r % G)
+  // ---- this wave's 32 query rows: row r <-> (node t = r / G, head g*G + r % G); their loads are issued
+  // before the item's metadata, so both are in flight together
   const int rend = min(R, (rg + 1) * group_rows);   // this row group's rows: [rg group_rows, rend)
   const int my_r = rg * group_rows + wave * 32 + (lane & 31);
   const bool row_ok = my_r < rend;
@@ -608,11 +606,14 @@ __device__ __forceinline__ void attn_item_dma(
       if (row_ok) z = *(const u32x4*)(qp + kq * 16 + half * 8);
       qf[kq] = z;
     }
-    // the K/V DMA below is invisible to the compiler's wait counting, so every compiler-tracked load
-    // must have landed before the first transfer is issued
-#pragma unroll
-    for (int kq = 0; kq < NQF; ++kq) asm volatile("" ::"v"(qf[kq]));
   }
+
+  const bool bad = attn_meta<D, 2>(meta, ctx_ok, last, page0, page1, block_table + (size_t)b * max_blocks,
+                                   parents + (size_t)b * T_, T_, Hkv, g, num_blocks);
+  // the K/V DMA below is invisible to the compiler's wait counting, so every compiler-tracked load must
+  // have landed before the first transfer is issued
+#pragma unroll
+  for (int kq = 0; kq < NQF; ++kq) asm volatile("" ::"v"(qf[kq]));
 
   f32x16 o[NDT];
 #pragma unroll
