@@ -119,6 +119,14 @@ def test_sweep_points_sampled(point):
     _compare(inp, rows=rows)
 
 
+@pytest.mark.parametrize("dt,top_p", [("bf16", 1.0), ("bf16", 0.95), ("f32", 1.0), ("f32", 0.95)])
+def test_largest_vocabulary(dt, top_p):
+    # V = 262144: 512 chunks of 512 tokens, the most a row may have; every trajectory compared
+    cfg = synth.scaled(synth.SHAPE_7B, B=6, T=16, depth=4, V=262144, dtype=dt)
+    _compare(synth.accept_inputs(cfg, seed=17), top_p=top_p)
+    _compare(synth.accept_inputs(cfg, seed=18, target_std=8.0, noise_std=0.05), top_p=top_p)
+
+
 def test_largest_tree():
     # SR_MAX_TREE = 128 nodes at depth 6 (the root has 43 children), every trajectory compared
     cfg = synth.scaled(synth.SHAPE_7B, B=24, T=128, depth=6, V=4096)

@@ -69,10 +69,14 @@ def test_config0_full():
     _check_fused_tree(inp, tok, cl, lg, range(inp["cfg"].B))
 
 
-# B*H rows 15, 96 and 132 take the 64-, 128- and 256-row vocabulary tiles
+# B*H rows 15, 96 and 132 take the 64-, 128- and 256-row vocabulary tiles; V = 262144 is the largest vocabulary
+# of the grouped top-M (4096 groups of 64 columns)
 @pytest.mark.parametrize("cfg_over", [dict(B=5, d=512, H=3, V=3000, T=16, depth=4),
                                       dict(B=24, d=512, H=4, V=5000, T=16, depth=4),
-                                      dict(B=33, d=256, H=4, V=1000, T=32, depth=5, active_frac=0.5)])
+                                      dict(B=33, d=256, H=4, V=1000, T=32, depth=5, active_frac=0.5),
+                                      dict(B=3, d=256, H=2, V=262144, T=24, depth=4),
+                                      dict(B=66, d=256, H=2, V=262144, T=16, depth=4)],
+                         ids=["B5-V3000", "B24-V5000", "B33-V1000", "B3-V262144", "B66-V262144"])
 def test_bf16_scaled(cfg_over):
     cfg = synth.scaled(synth.SHAPE_7B, **cfg_over)
     inp = synth.heads_inputs(cfg, seed=1)
@@ -132,7 +136,8 @@ def _gpu_tree(inp):
 
 
 @pytest.mark.parametrize("cfg", [synth.TINY_FP32, synth.scaled(synth.SHAPE_14B_TAIL, B=6, V=20000),
-                                 synth.scaled(synth.sweep_config(4, 96), V=50000)], ids=lambda c: c.name)
+                                 synth.scaled(synth.sweep_config(4, 96), V=50000),
+                                 synth.scaled(synth.SHAPE_7B, B=3, V=262144)], ids=lambda c: f"{c.name}-V{c.V}")
 @pytest.mark.parametrize("tie_frac", [0.0, 0.5])
 def test_tree_build_bit_exact(cfg, tie_frac):
     inp = synth.head_logits_inputs(cfg, seed=2, tie_frac=tie_frac)
