@@ -99,6 +99,8 @@ struct AccSmem {
   double nk_margin;
   unsigned long long nk_above, nk_bin;
   int nk_b;
+  int nk_found;
+  unsigned long long wtot[ACC_NW];   // per-wave totals of a block scan
   float wred[ACC_NW];        // per-wave partial of a block reduction
 };
 
@@ -233,7 +235,14 @@ __device__ __forceinline__ double ptilde(const AccSmem& sm, const T* row, int v,
 }
 
 // ---- nucleus truncation
-__device__ __forceinline__ unsigned long long nuc_fixed(float w) { return (unsigned long long)((double)w * NUC_FP); }
+// floor(w 2^40) for a weight w in [0, 1], from the float's bits: w 2^40 = m 2^e with m the 24-bit significand
+// (the same value as the float64 product truncated, without the conversions)
+__device__ __forceinline__ unsigned long long nuc_fixed(float w) {
+  const uint32_t u = __float_as_uint(w);
+  const int e = (int)(u >> 23) - 110;
+  const unsigned long long m = (unsigned long long)((u & 0x7fffffu) | 0x800000u);
+  return e >= 0 ? (m << e) : (e > -24 ? (m >> -e) : 0ull);
+}
 
 // Histogram of the fixed-point masses of the tokens whose key matches prefix under pmask, by key digit
 // (key >> sh) & dmask. Whole block.
@@ -387,12 +396,21 @@ __device__ void nuc_tie_cut(AccSmem& sm, const T* __restrict__ row, int V, uint3
 // second computes each token's weight once, for both the chunk sums (cmax[c] = M, cscale[c] = 1) and the
 // first digit of the nucleus histogram (the masses nuc_hist's first pass adds, in the same fixed point).
 // Leaves what row_stats leaves, plus that histogram. Whole block.
+// hc: NUC_HC copies of the first digit's histogram, lane l adding to copy l mod NUC_HC (a quarter of the
+// same-address collisions of one atomic instruction), summed into sm.nh at the end; null: sm.nh directly
+constexpr int NUC_HC = 4;
 template <typename T>
-__device__ void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, float invtau) {
+__device__ __attribute__((noinline)) void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, float invtau,
+                                                        unsigned long long* __restrict__ hc) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
   constexpr int GRP = RowLoad<T>::GROUP;
-  for (int i = tid; i < NUC_NB; i += ACC_NT) sm.nh[i] = 0ull;
+  if (hc != nullptr) {
+    for (int i = tid; i < NUC_HC * NUC_NB; i += ACC_NT) hc[i] = 0ull;
+  } else {
+    for (int i = tid; i < NUC_NB; i += ACC_NT) sm.nh[i] = 0ull;
+  }
+  unsigned long long* hist = hc != nullptr ? hc + (lane & (NUC_HC - 1)) * NUC_NB : sm.nh;
   auto load_group = [&](int c0, typename RowLoad<T>::Raw (&w)[GRP]) {
 #pragma unroll
     for (int gi = 0; gi < GRP; ++gi) {
@@ -434,7 +452,7 @@ __device__ void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, flo
         for (int e = 0; e < 8; ++e) {
           const float wt = tilt(x[e], invtau, M);
           a[gi] += wt;
-          if (x[e] != -INFINITY) atomicAdd(&sm.nh[acc_key(x[e]) >> 21], nuc_fixed(wt));
+          if (x[e] != -INFINITY) atomicAdd(&hist[acc_key(x[e]) >> 21], nuc_fixed(wt));
         }
       }
     }
@@ -443,6 +461,14 @@ __device__ void row_stats_nuc(AccSmem& sm, const T* __restrict__ row, int V, flo
     if ((lane & (64 / GRP - 1)) == 0 && c0 + j < nch) { sm.cmax[c0 + j] = M; sm.csum[c0 + j] = (double)sc; }
   }
   __syncthreads();
+  if (hc != nullptr) {                          // integer sums: the copies add up exactly
+    for (int i = tid; i < NUC_NB; i += ACC_NT) {
+      unsigned long long t = 0;
+#pragma unroll
+      for (int k = 0; k < NUC_HC; ++k) t += hc[k * NUC_NB + i];
+      sm.nh[i] = t;
+    }
+  }
   if (wave == 0) {
     double sl = 0.0;
     for (int c = lane; c < nch; c += 64) {
@@ -522,10 +548,16 @@ __device__ __attribute__((noinline)) void nucleus(AccSmem& sm, const T* __restri
 // weight (fp32; every cell is updated by the one wave that owns its chunk) and the token count (two 16-bit
 // counts per word; a chunk holds at most 512 tokens).
 constexpr int NUC_D2 = 32;                   // values of the second digit of a bf16 key (bits 16..20)
-struct NucBins {
+struct alignas(16) NucBins {
   float bm[ACC_MAX_CHUNKS * NUC_D2];
   uint32_t bc[ACC_MAX_CHUNKS * NUC_D2 / 2];
 };
+static_assert(sizeof(NucBins) >= NUC_HC * NUC_NB * sizeof(unsigned long long), "histogram copies fit the bins");
+// the bf16 nucleus pass's bins, which also hold the histogram copies of row_stats_nuc (used one after the other)
+__device__ __forceinline__ NucBins& nuc_bins() {
+  __shared__ NucBins nb;
+  return nb;
+}
 __device__ __forceinline__ int nuc_bcount(const NucBins& nb, int c, int d) {
   return (int)((nb.bc[c * (NUC_D2 / 2) + (d >> 1)] >> (16 * (d & 1))) & 0xffffu);
 }
@@ -542,19 +574,39 @@ __device__ __attribute__((noinline)) void nucleus_bf16(AccSmem& sm, NucBins& nb,
                              float top_p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = (V + ACC_CH - 1) / ACC_CH;
-  // total mass, target and the first digit's cut bin, from row_stats_nuc's histogram
-  if (wave == 0) {
-    unsigned long long ls = 0;
-    for (int b = lane; b < NUC_NB; b += 64) ls += sm.nh[b];
+  // total mass, target and the first digit's cut bin, from row_stats_nuc's histogram: one block scan with
+  // the bins in descending order (thread t holds bins NUC_NB-1-2t and NUC_NB-2-2t); the bin found is the one
+  // nuc_find would find over all NUC_NB bins
+  static_assert(NUC_NB == 2 * ACC_NT, "two bins per thread");
+  const int bhi = NUC_NB - 1 - 2 * tid;
+  const unsigned long long m0 = sm.nh[bhi], m1 = sm.nh[bhi - 1], v01 = m0 + m1;
+  unsigned long long incl = v01;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ls += __shfl_xor(ls, o, 64);
-    if (lane == 0) sm.nk_above = ls;          // stash the total
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) sm.wtot[wave] = incl;
+  if (tid == 0) sm.nk_found = 0;
+  __syncthreads();
+  unsigned long long total = 0, wbefore = 0;
+#pragma unroll
+  for (int w = 0; w < ACC_NW; ++w) {
+    const unsigned long long t = sm.wtot[w];
+    total += t;
+    wbefore += w < wave ? t : 0ull;
+  }
+  const unsigned long long target = (unsigned long long)ceil((double)top_p * (double)total);
+  {
+    const unsigned long long before = wbefore + incl - v01;   // mass of the bins above bhi
+    if (before < target && target <= before + m0) {
+      sm.nk_b = bhi; sm.nk_above = before; sm.nk_bin = m0; sm.nk_found = 1;
+    } else if (before + m0 < target && target <= before + v01) {
+      sm.nk_b = bhi - 1; sm.nk_above = before + m0; sm.nk_bin = m1; sm.nk_found = 1;
+    }
   }
   __syncthreads();
-  const unsigned long long total = sm.nk_above;
-  const unsigned long long target = (unsigned long long)ceil((double)top_p * (double)total);
-  __syncthreads();
-  if (wave == 0) nuc_find(sm, NUC_NB, 0ull, target);
+  if (tid == 0 && !sm.nk_found) { sm.nk_b = 0; sm.nk_above = 0ull; sm.nk_bin = 0ull; }   // an empty row
   __syncthreads();
   const uint32_t b1 = (uint32_t)sm.nk_b;
   const unsigned long long above1 = sm.nk_above;
@@ -985,10 +1037,14 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
   const int nch = (V + ACC_CH - 1) / ACC_CH;
   // nucleus cut of a row and its masked chunk sums: one fused pass for bf16 rows, two (plus the tie count
   // when the cut splits a key) for fp32 rows, whose keys take three digits
+  // weights and the first digit's histogram of a nucleus row (bf16: in copies held by the cut's bins)
+  auto nuc_stats = [&](const T* r) __attribute__((always_inline)) {
+    if constexpr (sizeof(T) == 2) row_stats_nuc<T>(sm, r, V, invtau, (unsigned long long*)&nuc_bins());
+    else row_stats_nuc<T>(sm, r, V, invtau, nullptr);
+  };
   auto nuc_cut = [&](const T* r) __attribute__((always_inline)) {
     if constexpr (NUC && sizeof(T) == 2) {
-      __shared__ NucBins nb;
-      nucleus_bf16(sm, nb, r, V, invtau, top_p);
+      nucleus_bf16(sm, nuc_bins(), r, V, invtau, top_p);
     } else {
       nucleus<T>(sm, r, V, invtau, top_p);
       nuc_masked_sums<T>(sm, r, V, invtau);
@@ -1022,7 +1078,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     __syncthreads();
     const int m = sm.nkid;
     if constexpr (NUC) {
-      row_stats_nuc<T>(sm, row, V, invtau);
+      nuc_stats(row);
       nuc_cut(row);                             // and the chunk sums over the nucleus
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
       outside_mass<T, NUC>(sm, row, V, invtau, m);   // sums the masked chunk sums to S
@@ -1113,7 +1169,7 @@ __global__ __launch_bounds__(ACC_NT) void k_tree_accept(const T* __restrict__ lo
     // accepted leaf: bonus token from its own target distribution
     const T* lrow = base + (size_t)c * V;
     if constexpr (NUC) {
-      row_stats_nuc<T>(sm, lrow, V, invtau);
+      nuc_stats(lrow);
       nuc_cut(lrow);
       if (tid == 0) margin = fmin(margin, sm.nk_margin);
     } else {
