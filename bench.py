@@ -71,6 +71,40 @@ def algorithmic(cfg, ctx_len, kernel):
     return dict(bytes=float("nan"), flops=float("nan"))
 
 
+def attn_chunks(cfg, ctx_len):
+    """Prefix chunks of every trajectory under the library's chunk plan (sr_tree_verify_attn): row groups of
+    at most 224 query rows (bf16), chunks of 32/128/256 pages by the number of (trajectory, KV head, row
+    group) triples."""
+    R = cfg.T * (cfg.Hq // cfg.Hkv)
+    ng = -(-R // 224) if (cfg.dtype == "bf16" and R > 224) else 1
+    triples = cfg.B * cfg.Hkv * ng
+    cp = 32 if triples < 64 else (128 if triples < 512 else 256)
+    pages = [-(-int(L) // cfg.block_size) for L in ctx_len]
+    return [max(1, -(-p_ // cp)) for p_ in pages], R
+
+
+def step_kernel_work(cfg, ctx_len, max_children, rows_read):
+    """Bytes and flops each step kernel moves or computes by design (one launch), for the per-kernel roofline.
+    The chunk merge moves the partial results the split prefix needs (not the method's own bytes); the
+    fp32-V recomputation has nothing to do on these inputs."""
+    B, T, Hq, Hkv, D, d, H, V = cfg.B, cfg.T, cfg.Hq, cfg.Hkv, cfg.D, cfg.d, cfg.H, cfg.V
+    e = 2 if cfg.dtype == "bf16" else 4
+    mc, G = int(max_children), -(-V // 64)
+    nch, R = attn_chunks(cfg, ctx_len)
+    merged = [c for c in nch if c > 1]
+    n_items = sum(nch) * Hkv * (-(-R // 224) if (cfg.dtype == "bf16" and R > 224) else 1)
+    w = {k: algorithmic(cfg, ctx_len, k) for k in ("sr_head_gemm", "sr_vocab_gemm", "sr_tree_attn")}
+    w["sr_clip_ln"] = dict(bytes=B * d * (e + 4 + 4 + e) + B, flops=12.0 * B * d)
+    w["sr_topm"] = dict(bytes=B * H * (G * 4 + mc * 64 * 4 + mc * 8), flops=float(B * H * (G + mc * 64)))
+    w["sr_tree_build"] = dict(bytes=B * H * mc * 8 + B * T * (4 + 4 + 4 + 8) + B * 4, flops=float(B * T * mc * 8))
+    w["sr_attn_order"] = dict(bytes=B * 4 + n_items * 8, flops=0.0)
+    w["sr_attn_redo"] = dict(bytes=4.0, flops=0.0)
+    w["sr_attn_combine"] = dict(bytes=sum(Hkv * (c * R * (D * 4 + 8) + R * (D * 4 + 4)) for c in merged),
+                                flops=float(sum(Hkv * c * R * D * 3 for c in merged)))
+    w["sr_tree_accept"] = dict(bytes=float(rows_read) * V * e + B * T * 16, flops=float(rows_read) * V * 4)
+    return w
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,6 +264,18 @@ def main():
                         "GB/s": a["bytes"] / (kms / 1e3) / 1e9,
                         "frac_hbm_peak": a["bytes"] / (kms / 1e3) / 1e9 / HBM_PEAK_GBPS}
 
+    # per-kernel roofline of one step: max(bytes / HBM peak, flops / bf16 MFMA peak) / measured time
+    kwork = step_kernel_work(cfg, ain["ctx_len"], hin["max_children"], rows_read)
+    kroof = {}
+    for k, ms in per_kernel.items():
+        wk = kwork.get(k)
+        if wk is None or not ms:
+            continue
+        t_hbm = wk["bytes"] / (HBM_PEAK_GBPS * 1e9)
+        t_mfma = wk["flops"] / (BF16_PEAK_TFLOPS * 1e12)
+        kroof[k] = {"ms": ms, "bytes": wk["bytes"], "flops": wk["flops"], "bound": "hbm" if t_hbm >= t_mfma else "mfma",
+                    "frac": max(t_hbm, t_mfma) / (ms / 1e3)}
+
     res = {
         "metric": METRIC, "value": value, "unit": "tree tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
@@ -249,6 +295,7 @@ def main():
         "head_gemms": gemms,
         "mall_check": mall,
         "kernels_ms": per_kernel,
+        "kernel_roofline": kroof,
         "accepted_mean_len": float(outs["out_len"].float().mean().item()),
     }
 
