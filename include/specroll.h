@@ -104,7 +104,7 @@ typedef struct {
   int32_t B;             /* trajectories, >= 1                                */
   int32_t d;             /* hidden size, multiple of 64                       */
   int32_t H;             /* future-token heads, >= 1                          */
-  int32_t V;             /* vocabulary, >= max_children                       */
+  int32_t V;             /* vocabulary, a multiple of 8, >= max_children      */
   int32_t T;             /* tree nodes incl. the root, 1..SR_MAX_TREE         */
   int32_t max_children;  /* upper bound on any node's child count, 0..T-1     */
   sr_dtype dtype;        /* element type of hidden, A, bias, W and z          */

@@ -102,7 +102,9 @@ static sr_status check_heads_desc(const sr_heads_desc* d, bool tree_only) {
   SR_CHECK(d != nullptr, "null descriptor");
   SR_CHECK(d->B >= 1, "B must be >= 1 (got %d)", d->B);
   SR_CHECK(d->H >= 1, "H must be >= 1 (got %d)", d->H);
-  SR_CHECK(d->V >= 1, "V must be >= 1 (got %d)", d->V);
+  // logits rows are written four columns per store: whole quads per row (the acceptance walk and the
+  // feedback take multiples of 8 of the same vocabulary)
+  SR_CHECK(d->V >= 8 && d->V % 8 == 0, "V must be a positive multiple of 8 (got %d)", d->V);
   SR_CHECK(d->T >= 1 && d->T <= SR_MAX_TREE, "T must be in [1, %d] (got %d)", SR_MAX_TREE, d->T);
   SR_CHECK(d->max_children >= 0 && d->max_children <= d->T - 1, "max_children must be in [0, T-1] (got %d)",
            d->max_children);

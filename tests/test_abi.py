@@ -50,7 +50,8 @@ def _call_heads(desc, **ptrs):
 
 
 @pytest.mark.parametrize("field,value", [("B", 0), ("d", 96), ("H", 0), ("T", 0), ("T", 129),
-                                         ("max_children", 8), ("dtype", 7), ("clip_norm", 0.0)])
+                                         ("max_children", 8), ("dtype", 7), ("clip_norm", 0.0),
+                                         ("V", 4099), ("V", 4), ("V", 0)])
 def test_heads_descriptor_rejected(field, value):
     desc = _lib.HeadsDesc(2, 256, 2, 512, 8, 2, _lib.SR_F32, 1.0, 1e-5)
     setattr(desc, field, value)

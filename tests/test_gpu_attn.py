@@ -79,6 +79,14 @@ def test_fp32_d128_and_bf16_d64():
                              seed=5))
 
 
+def test_one_query_head_per_kv_head():
+    # G = 1 (no grouping): one 32-row block per T nodes, split prefixes with ragged tails, bf16 and fp32
+    _check(synth.attn_inputs(synth.scaled(synth.SHAPE_7B, B=6, T=32, Hq=4, Hkv=4, ctx=("uniform", 900, 5000)),
+                             seed=11))
+    _check(synth.attn_inputs(synth.scaled(synth.SHAPE_7B, dtype="f32", B=3, T=16, Hq=2, Hkv=2,
+                                          ctx=("uniform", 100, 3000)), seed=12))
+
+
 def test_empty_prefix_and_single_node_tree():
     _check(synth.attn_inputs(synth.scaled(synth.TINY_FP32, ctx=("explicit", (0, 17))), seed=6))
     _check(synth.attn_inputs(synth.scaled(synth.TINY_FP32, T=1, parents=(-1,), ctx=("explicit", (0, 2049))),

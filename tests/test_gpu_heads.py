@@ -70,13 +70,16 @@ def test_config0_full():
 
 
 # B*H rows 15, 96 and 132 take the 64-, 128- and 256-row vocabulary tiles; V = 262144 is the largest vocabulary
-# of the grouped top-M (4096 groups of 64 columns)
+# of the grouped top-M (4096 groups of 64 columns); d = 64 is a single K-step of both GEMMs and d = 8192 the
+# widest row the clip + LayerNorm holds in registers
 @pytest.mark.parametrize("cfg_over", [dict(B=5, d=512, H=3, V=3000, T=16, depth=4),
                                       dict(B=24, d=512, H=4, V=5000, T=16, depth=4),
                                       dict(B=33, d=256, H=4, V=1000, T=32, depth=5, active_frac=0.5),
                                       dict(B=3, d=256, H=2, V=262144, T=24, depth=4),
-                                      dict(B=66, d=256, H=2, V=262144, T=16, depth=4)],
-                         ids=["B5-V3000", "B24-V5000", "B33-V1000", "B3-V262144", "B66-V262144"])
+                                      dict(B=66, d=256, H=2, V=262144, T=16, depth=4),
+                                      dict(B=9, d=64, H=3, V=4104, T=16, depth=4),
+                                      dict(B=3, d=8192, H=1, V=2048, T=8, depth=3)],
+                         ids=["B5-V3000", "B24-V5000", "B33-V1000", "B3-V262144", "B66-V262144", "d64", "d8192"])
 def test_bf16_scaled(cfg_over):
     cfg = synth.scaled(synth.SHAPE_7B, **cfg_over)
     inp = synth.heads_inputs(cfg, seed=1)
