@@ -15,7 +15,7 @@ whole step is timed on the other workloads (1.5B-shaped, 14B-shaped tail, and th
 Workload: the 7B-shaped rollout step (B=128 trajectories, T=32-node trees, Hq=28, Hkv=4, D=128,
 hidden 3584, 4 heads, vocab 151936, contexts uniform in [1024, 8192], bf16).
 
-Prints one JSON line. ``--gpus`` above 1 is refused: this build runs on one GPU.
+Prints one JSON line. ``--gpus`` above 1 is refused: the benchmark runs on one GPU.
 """
 from __future__ import annotations
 
@@ -120,7 +120,7 @@ def main():
                          "reference point that scales the HBM byte counters of a profiler run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
 
     import numpy as np
