@@ -202,6 +202,17 @@ def test_deterministic():
         np.testing.assert_array_equal(a[k], b[k])
 
 
+def test_nucleus_deterministic():
+    # the cut's fixed-point histograms and the bin tallies (each cell written by the one wave owning its chunk)
+    # give the same bits on every run, min_margin included; a flat row puts many tokens in the cut bin
+    for kw in (dict(), dict(target_std=0.5)):
+        inp = synth.accept_inputs(synth.scaled(synth.SHAPE_7B, B=24), seed=19, **kw)
+        a = _gpu_accept(inp, top_p=0.95)
+        b = _gpu_accept(inp, top_p=0.95)
+        for k in a:
+            np.testing.assert_array_equal(a[k].view(np.uint8), b[k].view(np.uint8), err_msg=k)
+
+
 # ---------------------------------------------------------------- nucleus truncation
 @pytest.mark.parametrize("top_p", [0.95, 0.5])
 def test_nucleus_config0_and_scaled(top_p):
