@@ -1005,24 +1005,26 @@ static sr_status launch_vocab_t(const sr_heads_desc& d, const void* z, const voi
                                 hipStream_t s) {
   const int M = d.B * d.H;
   if constexpr (sizeof(T) == 2) {
-    // M = B*H rows: 256-row tiles (8 waves, 128x64 each) when there are enough rows to fill them; at
-    // small batches 128- or 64-row tiles (4 waves) so that the MFMA work does not outgrow the W stream
-    constexpr int BN = 256, BK = 32;
+    // M = B*H rows: 256 x 256 quarter tiles (k_gemm_q) when there are enough rows to fill them. At small
+    // batches the GEMM is a stream of W: 64- or 128-row tiles by 128 columns (four waves of 32 or 64 rows by
+    // 64 columns; a 60 or 64 KB ring, two blocks per CU), so that the vocabulary splits into enough tiles
+    // to keep every CU streaming to the end (256-column tiles at one block per CU left the last of three
+    // rounds two-thirds empty)
+    constexpr int BK = 32;
     EpiLogitsMax epi{logits, gmax, d.V, (d.V + 63) / 64};
-    const int tn = (d.V + BN - 1) / BN;
     if (M <= 64) {
       constexpr int BM = 64;
-      const int tm = (M + BM - 1) / BM;
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 1, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
+      const int tm = (M + BM - 1) / BM, tn = (d.V + 127) / 128;
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, 128, BK, 2, 2, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
                 dim3(256), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
     } else if (M <= 128) {
       constexpr int BM = 128;
-      const int tm = (M + BM - 1) / BM;
-      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, BN, BK, 1, 4, 5, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
+      const int tm = (M + BM - 1) / BM, tn = (d.V + 127) / 128;
+      SR_LAUNCH("sr_vocab_gemm", (k_gemm_dl<BM, 128, BK, 2, 2, 4, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm),
                 dim3(256), 0, s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
     } else {
-      constexpr int BM = 256;
-      const int tm = (M + BM - 1) / BM;
+      constexpr int BM = 256, BN = 256;
+      const int tm = (M + BM - 1) / BM, tn = (d.V + BN - 1) / BN;
       SR_LAUNCH("sr_vocab_gemm", (k_gemm_q<SR_GQ_STAGES, EpiLogitsMax>), dim3(((tn + 7) / 8) * 8 * tm), dim3(256), 0,
                 s, (const T*)z, (const T*)W, M, d.V, d.d, tm, tn, epi);
     }
