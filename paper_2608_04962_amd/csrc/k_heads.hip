@@ -986,6 +986,15 @@ static sr_status launch_heads_z_t(const sr_heads_desc& d, const void* hidden, co
   if constexpr (sizeof(T) == 2) {
     constexpr int BM = 64, BN = 64, BK = 64;
     EpiHead<T> epi{(const T*)bias, x, (T*)z, d.d, d.H};
+    if (d.B <= 32 && (d.H * d.d + BN - 1) / BN < 256) {
+      // the rows fit one 32-row tile and 64 x 64 tiles would leave CUs without a block: the GEMM streams the
+      // weights, and 32 x 32 one-wave tiles (four times the blocks) keep every CU streaming to the end; with
+      // two row tiles they would read the weights twice
+      const int tn = (d.H * d.d + 31) / 32;
+      SR_LAUNCH("sr_head_gemm", (k_gemm_dl<32, 32, BK, 1, 1, 4, EpiHead<T>>), dim3(((tn + 7) / 8) * 8), dim3(64), 0, s,
+                (const T*)n, (const T*)A, d.B, d.H * d.d, d.d, 1, tn, epi);
+      return SR_OK;
+    }
     const int tm = (d.B + BM - 1) / BM, tn = (d.H * d.d + BN - 1) / BN;
     dim3 grid(((tn + 7) / 8) * 8 * tm);
     SR_LAUNCH("sr_head_gemm", (k_gemm_dl<BM, BN, BK, 2, 2, 4, EpiHead<T>>), grid, dim3(256), 0, s, (const T*)n,
